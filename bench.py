@@ -1,0 +1,234 @@
+#!/usr/bin/env python3
+"""Benchmark of the SRT tree-speculative verification step on one MI355X.
+
+A step is one pass of the whole hot path over one batch: srt_draft (draft
+trees from the per-prompt caches) -> srt_tree_attn (tree-masked attention of
+every node over its paged context) -> srt_accept (acceptance walk with T=1
+Gumbel sampling) -> srt_trie_insert (emitted tokens appended to each
+sequence's stream).  Inputs are resident in HBM before timing starts.
+
+Default workload: the Qwen2.5-7B-shaped layer (256 sequences, 28 query / 4
+KV heads, head_dim 128, log-normal contexts with median 4k and max 32k,
+64-node draft trees of depth <= 12, vocab 152064), synthetic.
+
+Prints one JSON line: tree tokens verified per second over the step, the
+roofline position of the dominant kernel (tree attention; events on its
+stream over the timed region) and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verified draft-tree tokens/sec + tree-attn HBM GB/s (% peak) at 1 GPU"
+HBM_PEAK_GBPS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+COUNTERS = os.path.join(ROOT, "profiles", "tree_attn_qwen7b_counters.json")
+ATTN_SRC = os.path.join(ROOT, "paper_2601_09083_amd", "csrc", "tree_attn.hip")
+
+
+def attn_work(cfg, ctx_len, tree_np):
+    """Algorithmic bytes and FLOPs of one tree-attention launch: every K/V
+    position of every sequence read once (context + tree), Q read once, O
+    written once; 4*d FLOPs per (query row, visible key)."""
+    n = tree_np["n_nodes"].astype(np.int64)
+    L = ctx_len.astype(np.int64)
+    d, hq, hkv = cfg.head_dim, cfg.hq, cfg.hkv
+    kv_bytes = int(((L + n) * hkv * d * 2 * 2).sum())
+    qo_bytes = int((n * hq * d * 2 * 2).sum())
+    depth = tree_np["tree_depth"]
+    vis = 0
+    for b in range(len(n)):
+        vis += int(n[b]) * int(L[b]) + int((depth[b, : n[b]] + 1).sum())
+    flops = 4 * d * hq * vis
+    return kv_bytes + qo_bytes, flops
+
+
+def source_sha(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def counter_traffic():
+    """HBM bytes per launch from committed rocprofv3 counters, if they were
+    taken on the current kernel source."""
+    if not os.path.exists(COUNTERS):
+        return None
+    try:
+        c = json.load(open(COUNTERS))
+        if c.get("source_sha256") != source_sha(ATTN_SRC):
+            return None
+        return c.get("hbm_bytes_per_launch")
+    except Exception:
+        return None
+
+
+def cpu_baseline(st, tree_np, budget_s: float):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    per sequence the draft (from the prompt's stream index), fp64 tree
+    attention, the acceptance walk and the online insert; 1 thread."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import accept as AC
+    from oracle import attention as AT
+    from oracle import draft as DR
+    from oracle import trie as TR
+
+    cfg, tw = st.cfg, st.tokens
+    tails, ts = tw.ctx_tail(), tw.draft_len()
+    order = np.random.default_rng(7).permutation(tw.batch)
+    tries = {}
+    t_total, tok_total, seqs = 0.0, 0, 0
+    with threadpool_limits(limits=1):
+        for b in order:
+            b = int(b)
+            p = int(tw.seq_prompt[b])
+            if p not in tries:
+                tries[p] = TR.StreamTrie(tw.streams_of_prompt(p), cfg.trie_depth)
+            # inputs staged to host memory outside the timed region
+            L = int(tw.ctx_len[b])
+            N = cfg.n_nodes
+            npg = (L + N + cfg.page - 1) // cfg.page
+            pages = st.block_table[b, :npg].long()
+            kc = st.k_cache[pages].float().cpu().numpy()
+            vc = st.v_cache[pages].float().cpu().numpy()
+            q = st.q[b].float().cpu().numpy()
+            logits = st.logits[b].cpu().numpy()
+            noise = st.gumbel[b].cpu().numpy() if st.gumbel is not None else None
+            t0 = time.perf_counter()
+            tok, par, dep, n, qm = DR.draft(tries[p], tails[b], int(ts[b]), cfg.max_match, N, cfg.max_depth)
+            AT.tree_attention_seq(q, kc, vc, np.arange(npg), L, par, n, st.scale, cfg.page)
+            k, out, nodes = AC.accept(lambda u: logits[u], (lambda s: noise[s]) if noise is not None else None,
+                                      1.0, tok, par, n, cfg.max_depth)
+            TR.insert_counts({}, tw.seqs[b][-cfg.trie_depth:], out, cfg.trie_depth)
+            t_total += time.perf_counter() - t0
+            tok_total += n
+            seqs += 1
+            if t_total >= budget_s:
+                break
+    return {"value": tok_total / t_total, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{seqs} of {tw.batch} sequences of the {cfg.name} workload, one step each "
+                      f"(draft + fp64 tree attention + acceptance + insert), {t_total:.1f} s on 1 thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="qwen7b")
+    ap.add_argument("--greedy", action="store_true", help="greedy acceptance instead of T=1 sampling")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
+              f"(the path shards per prompt, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2601_09083_amd import workload as W
+    from paper_2601_09083_amd.pipeline import VerifyState
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    cfg = W.CONFIGS[args.config]
+    t_setup = time.perf_counter()
+    st = VerifyState.build(cfg, steps_headroom=args.steps + args.warmup + 4)
+    st.draft()
+    st.make_logits(sampled=not args.greedy)
+    torch.cuda.synchronize()
+    t_setup = time.perf_counter() - t_setup
+    print(f"# setup {t_setup:.1f}s: {cfg.name}, B={st.tokens.batch}", file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        st.step()
+    torch.cuda.synchronize()
+
+    parts = ("draft", "attention", "accept", "insert")
+    ev = {p: [] for p in parts}
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        for p in parts:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            getattr(st, p)()
+            e1.record(stream)
+            ev[p].append((e0, e1))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    part_ms = {p: float(np.mean([a.elapsed_time(b) for a, b in ev[p]])) for p in parts}
+
+    tree_np = {k: v.cpu().numpy() for k, v in st.tree.items()}
+    acc_np = {k: v.cpu().numpy() for k, v in st.acc.items()}
+    n_tree = int(tree_np["n_nodes"].sum())
+    n_emit = int(acc_np["n_emitted"].sum())
+    ms_step = wall * 1e3 / args.steps
+    value = n_tree / (ms_step / 1e3)
+
+    nbytes, flops = attn_work(cfg, st.tokens.ctx_len, tree_np)
+    t_attn = part_ms["attention"] / 1e3
+    t_hbm, t_mfma = nbytes / (HBM_PEAK_GBPS * 1e9), flops / (BF16_PEAK_TFLOPS * 1e12)
+    if t_mfma >= t_hbm:
+        roof = {"bound": "mfma", "achieved": flops / t_attn / 1e12, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": nbytes / t_attn / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = counter_traffic()
+    roof["kernel"] = "srt_tree_attn (tree_attn_kernel + tree_attn_combine_kernel)"
+    roof["algorithmic_bytes"] = nbytes
+    roof["algorithmic_flops"] = flops
+    roof["launch_ms"] = part_ms["attention"]
+    attn_hbm = nbytes / t_attn / 1e9
+
+    res = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg.name}: {st.tokens.batch} sequences, Hq {cfg.hq}/Hkv {cfg.hkv}/d {cfg.head_dim}, "
+                         f"contexts {cfg.ctx_len.kind}({cfg.ctx_len.a},{cfg.ctx_len.b}), draft trees N={cfg.n_nodes} "
+                         f"Dmax={cfg.max_depth}, vocab {cfg.vocab}, "
+                         f"{'greedy' if args.greedy else 'T=1 Gumbel'} acceptance, caches of "
+                         f"{cfg.rollouts_per_prompt} prior rollouts/prompt"),
+            "global_batch": st.tokens.batch,
+            "seq_len": int(st.tokens.ctx_len.max()),
+            "mean_ctx": float(st.tokens.ctx_len.mean()),
+            "parallelism": "none (1 GPU)",
+        },
+        "tree_attn_hbm": {"achieved_GBps": attn_hbm, "peak_GBps": HBM_PEAK_GBPS, "frac": attn_hbm / HBM_PEAK_GBPS},
+        "parts_ms": part_ms,
+        "accepted_tokens_per_s": n_emit / (ms_step / 1e3),
+        "mean_tree_nodes": n_tree / st.tokens.batch,
+        "mean_emitted": n_emit / st.tokens.batch,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(st, tree_np, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,208 @@
+/*
+ * srt.h -- C ABI of libsrt: the tree-speculative verification step of SRT
+ * (Speculative Rollout with Tree-Structured Cache, arXiv 2601.09083) on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * One verification step is
+ *   srt_draft      -> tree of drafted tokens from the per-prompt cache
+ *   (caller)       -> writes the tree's K/V into the paged cache, RoPE, ...
+ *   srt_tree_attn  -> attention of every tree node over context + ancestors
+ *   (caller)       -> LM head: per-node logits
+ *   srt_accept     -> accepted path + bonus token
+ *   srt_trie_insert-> emitted tokens appended to the sequence's stream
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are device pointers unless the comment says "host".  All
+ *     device memory is owned by the caller; the library allocates nothing
+ *     and keeps no global state.
+ *   - `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *     Every call only enqueues work on it and returns, except those marked
+ *     "synchronises".  Calls sharing a workspace must be ordered on one
+ *     stream (or by the caller).
+ *   - Return value: SRT_OK, or a negative srt_status.  Argument errors are
+ *     found on the host before anything is enqueued (SRT_ERR_INVALID /
+ *     SRT_ERR_UNSUPPORTED); launch failures give SRT_ERR_HIP.  Conditions
+ *     only the device can see (cache full, a stream bound to another prompt,
+ *     out-of-range ids) set sticky flags in the workspace, read with
+ *     srt_trie_status; the kernels never access memory outside the
+ *     documented extents, whatever the device-side values are.
+ *   - bf16 values travel as uint16_t bit patterns.
+ */
+#ifndef SRT_H_
+#define SRT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SRT_OK = 0,
+  SRT_ERR_INVALID = -1,      /* bad argument (host check) */
+  SRT_ERR_CAPACITY = -2,     /* workspace / output too small */
+  SRT_ERR_HIP = -3,          /* HIP runtime or launch error */
+  SRT_ERR_UNSUPPORTED = -4   /* valid but not implemented (e.g. head_dim) */
+} srt_status;
+
+/* Sticky device-side flags reported by srt_trie_status (bit mask). */
+#define SRT_FLAG_CAPACITY  1u  /* node table full: later inserts are dropped */
+#define SRT_FLAG_STREAM    2u  /* a stream id was out of range or bound to another prompt */
+#define SRT_FLAG_PROMPT    4u  /* a prompt id was out of range */
+
+/* ------------------------------------------------------------------------
+ * Per-prompt cache (Section 3, "Per-prompt rollout cache using
+ * tree-structured cache" and "Cache update strategy").
+ *
+ * The cache of prompt p holds count(s) for every token string s with
+ * 1 <= |s| <= max_depth that occurs in the streams inserted for p, where
+ * count(s) is the number of occurrences (stream, start position); no
+ * occurrence spans two streams.  A stream is one rollout (prior, running, or
+ * run-ahead) and is identified by a caller-chosen id < max_streams; it is
+ * bound to the prompt of its first insert.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  int32_t n_prompts;      /* number of per-prompt caches, >= 1 */
+  int32_t max_streams;    /* stream ids are 0..max_streams-1, >= 1 */
+  int32_t max_depth;      /* D: longest indexed substring, 1..64 */
+  int32_t reserved;       /* must be 0 */
+  int64_t node_capacity;  /* most nodes (strings) over all prompts, >= 1 */
+} srt_trie_config;
+
+/* Bytes of device memory the workspace needs for `cfg` (host only, no HIP
+ * call).  Returns 0 if `cfg` is invalid. */
+size_t srt_trie_workspace_bytes(const srt_trie_config* cfg);
+
+/* Formats `ws` (device, ws_bytes >= srt_trie_workspace_bytes(cfg), 256-byte
+ * aligned) as empty caches for every prompt and unbound streams. */
+int srt_trie_init(void* ws, size_t ws_bytes, const srt_trie_config* cfg, void* stream);
+
+/* Appends tokens to streams and updates the counts (online insertion).
+ * Entry i appends tokens[i*stride + 0 .. lengths[i]-1] to stream
+ * stream_ids[i] of prompt prompt_ids[i]: for each appended token at stream
+ * index j, every suffix of the stream ending at j of length <= D gains one
+ * occurrence.  Arrays: prompt_ids, stream_ids, lengths [n] int32; tokens
+ * [n, stride] int32 (tokens >= 0).  Stream ids must be distinct within one
+ * call.  n == 0 is a no-op.  Entries with an out-of-range prompt or stream,
+ * or a stream bound to another prompt, are skipped and flagged. */
+int srt_trie_insert(void* ws, int32_t n, const int32_t* prompt_ids, const int32_t* stream_ids,
+                    const int32_t* tokens, const int32_t* lengths, int32_t stride, void* stream);
+
+/* Unbinds streams so their ids can start new rollouts (of any prompt).  The
+ * counts they contributed stay in the cache.  stream_ids [n] int32. */
+int srt_trie_reset_streams(void* ws, int32_t n, const int32_t* stream_ids, void* stream);
+
+/* Synchronises.  info (host, [4] int64): flags (SRT_FLAG_*), nodes in use,
+ * node_capacity, hash-table slots.  Returns SRT_ERR_CAPACITY if the
+ * capacity flag is set, else SRT_OK. */
+int srt_trie_status(const void* ws, int64_t* info, void* stream);
+
+/* Synchronises.  Dumps the cache of `prompt_id` breadth-first: row r is one
+ * string s (depth 1 first), with parent[r] the row of s minus its last token
+ * (-1 at depth 1), token[r] its last token and count[r] = count(s).  The
+ * order of rows within a depth is unspecified.  Arrays (device) hold
+ * max_nodes rows.  *n_out (host) receives the number of strings; if it
+ * exceeds max_nodes only max_nodes rows are written and SRT_ERR_CAPACITY is
+ * returned.  Test and checkpoint hook, not on the hot path. */
+int srt_trie_export(const void* ws, int32_t prompt_id, int64_t max_nodes, int32_t* parent,
+                    int32_t* token, uint32_t* count, int64_t* n_out, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Draft extraction (Section 3, "Speculative Rollout with Tree-Structured
+ * Cache"; the edge score is the displayed equation there).
+ *
+ * For sequence b with t = ctx_len[b] committed tokens, the last
+ * min(t, max_match) of them right-aligned in ctx_tail[b, 0..max_match-1]:
+ *   q* = the longest q <= min(t, max_match) such that the last q tokens form
+ *        a string of the prompt's cache with at least one continuation;
+ *   u  = that string; q* = 0 means fall back to a one-node tree.
+ *   Candidates are the descendants v of u up to relative depth
+ *   min(max_depth, D - q*), with C(v) = count(v) / sum over the children w
+ *   of parent(v) of count(w) (one IEEE fp64 division) and
+ *   score(v) = score(parent(v)) * C(v) (one fp64 multiplication),
+ *   score(u) = 1.  They are ranked by score (descending), then relative
+ *   depth (ascending), then token path from u (lexicographic by token id),
+ *   and the first B are drafted, B = max_nodes - 1, or
+ *   min(max_nodes - 1, floor(budget_alpha * q*)) when budget_alpha > 0.
+ * Output tree (row-major [B, max_nodes] int32, rows >= n_nodes[b] set to -1):
+ *   node 0 = last committed token (ctx_tail[b, max_match-1], -1 if t == 0),
+ *   parent -1, depth 0; nodes 1.. = drafted nodes in rank order, each with
+ *   the index of its parent (< its own index) and its depth relative to u.
+ * n_nodes[b] = 1 + drafted, match_len[b] = q*.  Results are bit-identical
+ * across runs and launch shapes.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  int32_t max_match;     /* Qmax: 1..64, columns of ctx_tail */
+  int32_t max_nodes;     /* N: tree rows including the root, 1..256 */
+  int32_t max_depth;     /* Dmax: 0..63 */
+  int32_t reserved;      /* must be 0 */
+  double budget_alpha;   /* <= 0: budget N-1 */
+} srt_draft_params;
+
+int srt_draft(const void* ws, int32_t B, const int32_t* prompt_ids, const int32_t* ctx_tail,
+              const int32_t* ctx_len, const srt_draft_params* params, int32_t* tree_tokens,
+              int32_t* tree_parent, int32_t* tree_depth, int32_t* n_nodes, int32_t* match_len,
+              void* stream);
+
+/* ------------------------------------------------------------------------
+ * Tree-masked attention over a paged KV cache (Section 3: one decode pass
+ * verifies every drafted token; Appendix C: the KV cache is read once).
+ *
+ * For sequence b, query head h (KV head g = h / (Hq / Hkv)) and tree node
+ * i < n_nodes[b]:
+ *   keys = positions [0, L) and L + j for every ancestor-or-self j of i,
+ *   L = ctx_len[b]; position p lives in page block_table[b, p / page],
+ *   slot p % page;  out[b,i,h,:] = softmax(scale * q.K^T) V.
+ * Layouts (bf16 bits): q, out [B, N, Hq, d]; k_cache, v_cache
+ *   [num_pages, Hkv, page, d]; block_table [B, max_pages] int32;
+ *   ctx_len, n_nodes [B] int32; tree_parent [B, N] int32 as from srt_draft.
+ * Requirements: 1 <= n_nodes[b] <= N <= 256, parent[i] < i,
+ *   L + n_nodes[b] <= max_pages * page, block_table entries < num_pages for
+ *   the pages those positions use.  Values outside these ranges are clamped
+ *   or read as zero (never out of bounds); rows i >= n_nodes[b] of out are
+ *   not written.  d must be 64 or 128; Hq % Hkv == 0.
+ * scratch: device buffer of at least srt_tree_attn_scratch_bytes(...) bytes
+ * for split-context partial results (may be NULL if that returns 0).
+ * ---------------------------------------------------------------------- */
+size_t srt_tree_attn_scratch_bytes(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d,
+                                   int32_t page, int32_t max_pages);
+
+int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d, int32_t page,
+                  int32_t max_pages, int64_t num_pages, const uint16_t* q,
+                  const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* block_table,
+                  const int32_t* ctx_len, const int32_t* tree_parent, const int32_t* n_nodes,
+                  float scale, uint16_t* out, void* scratch, size_t scratch_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Acceptance walk (Sections 1 and 3: accept drafted tokens up to the first
+ * mismatch, which keeps the policy's distribution exactly).
+ *
+ * From u = root, step k = 0, 1, ...:
+ *   x_j = logits[b,u,j]                                   (gumbel == NULL)
+ *   x_j = fl(fl(logits[b,u,j] * inv_temperature) + gumbel[b,k,j])  (fp32)
+ *   tok = arg-max_j x_j, lowest j on ties;
+ *   if a child c of u (tree_parent[b,c] == u, c > u) has tree_tokens[b,c]
+ *   == tok and k < Dmax: accept it (out_tokens[b,k] = tok,
+ *   out_nodes[b,k] = c), u = c, next step; else out_tokens[b,k] = tok is
+ *   the bonus token, n_accepted[b] = k, stop.
+ * Layouts: logits [B, N, V] fp32; gumbel [B, Dmax+1, V] fp32 or NULL
+ * (greedy); tree_tokens, tree_parent [B, N] int32; n_nodes [B] int32;
+ * outputs n_accepted [B], out_tokens, out_nodes [B, Dmax+1] int32 (unused
+ * entries -1) and, if not NULL, n_emitted [B] = n_accepted + 1, the number
+ * of tokens the sequence appends (ready as `lengths` for srt_trie_insert
+ * with tokens = out_tokens, stride Dmax+1).  Inputs must be finite (results
+ * are unspecified otherwise).
+ * ---------------------------------------------------------------------- */
+int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits,
+               const float* gumbel, float inv_temperature, const int32_t* tree_tokens,
+               const int32_t* tree_parent, const int32_t* n_nodes, int32_t* n_accepted,
+               int32_t* out_tokens, int32_t* out_nodes, int32_t* n_emitted, void* stream);
+
+/* Library version string (host only). */
+const char* srt_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SRT_H_ */

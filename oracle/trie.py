@@ -98,3 +98,18 @@ class StreamTrie:
         nxt = nxt[nxt >= 0]
         xs, cs = np.unique(nxt, return_counts=True)
         return {int(x): int(c) for x, c in zip(xs, cs)}
+
+
+def insert_counts(counts: Dict[Tuple[int, ...], int], stream_before: Sequence[int], appended: Sequence[int],
+                  D: int) -> None:
+    """Online insertion (Section 3, "Cache update strategy"): appending token
+    x at index j of a stream adds one occurrence to every suffix of the
+    stream ending at j, of length 1..min(D, j+1).  Updates ``counts`` in
+    place; ``stream_before`` is the stream's content so far."""
+    st = [int(x) for x in stream_before]
+    for x in appended:
+        st.append(int(x))
+        j = len(st) - 1
+        for ell in range(1, min(D, j + 1) + 1):
+            key = tuple(st[j - ell + 1:j + 1])
+            counts[key] = counts.get(key, 0) + 1

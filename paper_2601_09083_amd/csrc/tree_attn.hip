@@ -1,0 +1,484 @@
+// Tree-masked attention over a paged bf16 KV cache (MFMA, gfx950).
+//
+// Method: Section 3 of the paper -- one decode pass of the policy verifies
+// every drafted token -- and Appendix C (verification reads the KV cache
+// once for all candidates).  Tree node i of sequence b attends to the whole
+// committed context [0, L) and to the tree positions L + j of its
+// ancestors-or-self j; query head h uses KV head h / (Hq / Hkv).
+//
+// GPU design.  For one (sequence, KV head) all n * G query rows (G query
+// heads per KV head) share every K/V tile, so they are processed together:
+// a workgroup of 4 waves owns 128 rows (32 per wave, two 16-row MFMA tiles)
+// and streams one split of the key range in 64-key tiles.
+//   * K and V tiles are read from HBM with 16-byte coalesced loads,
+//     prefetched into registers one tile ahead, and staged in LDS (V is
+//     transposed on the way in).
+//   * S^T = K Q^T and O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 with
+//     fp32 accumulation.  In this orientation a query row lives in one lane
+//     column of both accumulators, so the online-softmax statistics and the
+//     rescale of O are lane-local, and the probabilities P feed the second
+//     MFMA straight from registers: the contraction index of P^T is
+//     permuted to match the S^T output layout and V^T is read with the same
+//     permutation.
+//   * Softmax uses exp2 with scale*log2(e) folded in; row max and sum need
+//     two cross-lane shuffles.  The ancestor mask is a bitset per tree node
+//     in LDS and is applied only on tiles that reach the tree positions or
+//     the end of the range.
+//   * Long contexts are split into fixed chunks of keys so the grid has
+//     enough independent work; each split writes unnormalised partial
+//     output plus (max, sum) and a small combine kernel merges them.  A
+//     sequence that fits in one chunk writes bf16 output directly.
+//   * Block ids are remapped so that the row blocks and splits of one
+//     (sequence, KV head) run on the same XCD and share its L2.
+#include <cmath>
+
+#include "common.h"
+
+using namespace srt;
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * SRT_WAVE;
+constexpr int kRowsPerBlock = kWaves * 32;
+constexpr int kTile = 64;      // keys per tile
+constexpr int kMaxN = 256;     // tree rows
+constexpr int kChunk = 4096;   // keys per split
+constexpr int kXcds = 8;
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* bt;
+  const int32_t* ctx_len;
+  const int32_t* parent;
+  const int32_t* n_nodes;
+  uint16_t* out;
+  float* part_o;
+  float* part_ml;
+  int32_t B, N, Hq, Hkv, G, page, max_pages;
+  int64_t num_pages;
+  float scale_log2;
+  int32_t S, RB, total;
+};
+
+template <int D>
+struct Shape {
+  static constexpr int KS = D + 8;       // LDS row stride of the K tile (bf16 elements)
+  static constexpr int VS = kTile + 4;   // LDS row stride of the V^T tile
+  static constexpr int KD = D / 32;      // MFMA steps over the head dimension
+  static constexpr int DT = D / 16;      // 16-wide blocks of the head dimension
+  static constexpr int KCH = D / 32;     // 16-byte K chunks per thread per tile
+};
+
+__device__ inline uint16_t to_bf16_bits(float x) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x)); }
+
+struct SeqInfo {
+  int n, L, total;
+};
+
+__device__ inline SeqInfo seq_info(const AttnArgs& a, int b) {
+  SeqInfo s;
+  const int cap = a.max_pages * a.page;
+  s.n = min(max(a.n_nodes[b], 1), min(a.N, cap));
+  s.L = min(max(a.ctx_len[b], 0), cap - s.n);
+  s.total = s.L + s.n;
+  return s;
+}
+
+// Element offset of position `pos` of KV head g of sequence b, or -1.
+__device__ inline int64_t kv_offset(const AttnArgs& a, int b, int g, int pos, int D) {
+  const int pg = a.bt[static_cast<int64_t>(b) * a.max_pages + pos / a.page];
+  if (pg < 0 || pg >= a.num_pages) return -1;
+  return ((static_cast<int64_t>(pg) * a.Hkv + g) * a.page + pos % a.page) * D;
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
+  using Sh = Shape<D>;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kTile * Sh::KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * Sh::VS];
+  __shared__ uint64_t anc[kMaxN][4];
+  __shared__ int32_t spar[kMaxN];
+
+  const int nb = gridDim.x;
+  const int item = (blockIdx.x % kXcds) * (nb / kXcds) + blockIdx.x / kXcds;
+  if (item >= a.total) return;
+  int rest = item;
+  const int rb = rest % a.RB;
+  rest /= a.RB;
+  const int s = rest % a.S;
+  rest /= a.S;
+  const int g = rest % a.Hkv;
+  const int b = rest / a.Hkv;
+
+  const SeqInfo si = seq_info(a, b);
+  const int rows = si.n * a.G;
+  if (rb * kRowsPerBlock >= rows) return;
+  const int k_begin = s * kChunk;
+  if (k_begin >= si.total) return;
+  const int k_end = min(k_begin + kChunk, si.total);
+  const int nsplit = (si.total + kChunk - 1) / kChunk;
+
+  const int tid = threadIdx.x;
+  const int w = tid / SRT_WAVE;
+  const int lane = tid % SRT_WAVE;
+  const int l16 = lane % 16;
+  const int lg = lane / 16;
+
+  // Ancestor-or-self bitsets, needed only when this split reaches the tree.
+  if (k_end > si.L) {
+    for (int i = tid; i < si.n; i += kThreads) spar[i] = a.parent[static_cast<int64_t>(b) * a.N + i];
+    __syncthreads();
+    for (int i = tid; i < si.n; i += kThreads) {
+      uint64_t bits[4] = {0, 0, 0, 0};
+      int j = i;
+      while (j >= 0) {
+        bits[j >> 6] |= 1ull << (j & 63);
+        const int pj = spar[j];
+        if (pj >= j) break;  // malformed parent: stop (parents precede children)
+        j = pj;
+      }
+#pragma unroll
+      for (int x = 0; x < 4; ++x) anc[i][x] = bits[x];
+    }
+  }
+
+  // Query fragments: B operand of S^T = K Q^T (lane: row l16, head-dim 8*lg..+7).
+  bf16x8 qf[2][Sh::KD];
+  int node_of[2];
+  bool row_ok[2];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt) {
+    const int r = rb * kRowsPerBlock + w * 32 + nt * 16 + l16;
+    row_ok[nt] = r < rows;
+    const int node = row_ok[nt] ? r / a.G : 0;
+    const int h = g * a.G + (row_ok[nt] ? r % a.G : 0);
+    node_of[nt] = node;
+    const bf16x8* qp = reinterpret_cast<const bf16x8*>(
+        a.q + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + h) * D + 8 * lg);
+#pragma unroll
+    for (int kd = 0; kd < Sh::KD; ++kd) {
+      if (row_ok[nt]) {
+        qf[nt][kd] = qp[4 * kd];
+      } else {
+        qf[nt][kd] = bf16x8{};
+      }
+    }
+  }
+
+  f32x4 o[2][Sh::DT];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+    for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m[2] = {-INFINITY, -INFINITY};
+  float l[2] = {0.f, 0.f};
+
+  // Staging assignment.  K: chunk c = tid + 256*i covers key c / (D/8), part c % (D/8).
+  // V: d-octet od = tid % (D/8), key quad kq = tid / (D/8) (keys 4kq..4kq+3).
+  uint4 kreg[Sh::KCH];
+  uint4 vreg[4];
+  constexpr int kOct = D / 8;
+  constexpr int kVThreads = kOct * (kTile / 4);  // 256 for D=128, 128 for D=64
+  const int od = tid % kOct;
+  const int kq = tid / kOct;
+
+  auto load_tile = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < Sh::KCH; ++i) {
+      const int c = tid + kThreads * i;
+      const int key = c / kOct, part = c % kOct;
+      const int pos = t0 + key;
+      kreg[i] = make_uint4(0, 0, 0, 0);
+      if (pos < k_end) {
+        const int64_t off = kv_offset(a, b, g, pos, D);
+        if (off >= 0) kreg[i] = *reinterpret_cast<const uint4*>(a.k + off + part * 8);
+      }
+    }
+    if (tid < kVThreads) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int pos = t0 + 4 * kq + r;
+        vreg[r] = make_uint4(0, 0, 0, 0);
+        if (pos < k_end) {
+          const int64_t off = kv_offset(a, b, g, pos, D);
+          if (off >= 0) vreg[r] = *reinterpret_cast<const uint4*>(a.v + off + od * 8);
+        }
+      }
+    }
+  };
+
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < Sh::KCH; ++i) {
+      const int c = tid + kThreads * i;
+      const int key = c / kOct, part = c % kOct;
+      *reinterpret_cast<uint4*>(&Ks[key * Sh::KS + part * 8]) = kreg[i];
+    }
+    if (tid < kVThreads) {
+      // 4 keys x 8 dims -> 8 rows of V^T, 4 keys each.
+      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
+      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
+      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
+      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int sh = (e & 1) * 16;
+        const uint32_t a0 = (w0[e >> 1] >> sh) & 0xFFFFu, a1 = (w1[e >> 1] >> sh) & 0xFFFFu;
+        const uint32_t a2 = (w2[e >> 1] >> sh) & 0xFFFFu, a3 = (w3[e >> 1] >> sh) & 0xFFFFu;
+        *reinterpret_cast<uint2*>(&Vt[(8 * od + e) * Sh::VS + 4 * kq]) = make_uint2(a0 | (a1 << 16), a2 | (a3 << 16));
+      }
+    }
+  };
+
+  const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
+  load_tile(k_begin);
+  for (int it = 0; it < ntiles; ++it) {
+    const int t0 = k_begin + it * kTile;
+    store_tile();
+    __syncthreads();
+    if (it + 1 < ntiles) load_tile(t0 + kTile);
+
+    // S^T[key][row] for 4 key groups x 2 row tiles.
+    f32x4 sacc[2][4];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) sacc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kd = 0; kd < Sh::KD; ++kd) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&Ks[(16 * mt + l16) * Sh::KS + 32 * kd + 8 * lg]);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+          sacc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[nt][kd], sacc[nt][mt], 0, 0, 0);
+      }
+    }
+
+    // Mask, online softmax, P in bf16.
+    const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float x = sacc[nt][mt][r] * a.scale_log2;
+          if (need_mask) {
+            const int pos = t0 + 16 * mt + 4 * lg + r;
+            bool vis = pos < k_end;
+            if (vis && pos >= si.L) {
+              const int j = pos - si.L;
+              vis = (anc[node_of[nt]][j >> 6] >> (j & 63)) & 1ull;
+            }
+            if (!vis) x = -INFINITY;
+          }
+          sacc[nt][mt][r] = x;
+          mloc = fmaxf(mloc, x);
+        }
+      }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, SRT_WAVE));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, SRT_WAVE));
+      const float mnew = fmaxf(m[nt], mloc);
+      const bool dead = mnew == -INFINITY;
+      const float alpha = dead ? 1.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
+      float psum = 0.f;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = dead ? 0.f : __builtin_amdgcn_exp2f(sacc[nt][mt][r] - mnew);
+          sacc[nt][mt][r] = p;
+          psum += p;
+        }
+      }
+      l[nt] = l[nt] * alpha + psum;
+      m[nt] = mnew;
+#pragma unroll
+      for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] *= alpha;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pb[nt][ks][r] = static_cast<__bf16>(sacc[nt][2 * ks][r]);
+          pb[nt][ks][4 + r] = static_cast<__bf16>(sacc[nt][2 * ks + 1][r]);
+        }
+      }
+    }
+
+    // O^T[d][row] += V^T P^T; contraction index (8*lg + e) <-> key
+    // 32*ks + 16*(e/4) + 4*lg + e%4, matching the S^T output layout.
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+      for (int dt = 0; dt < Sh::DT; ++dt) {
+        const uint16_t* vp = &Vt[(16 * dt + l16) * Sh::VS + 32 * ks + 4 * lg];
+        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 16);
+        const uint4 packed = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        const bf16x8 va = __builtin_bit_cast(bf16x8, packed);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+          o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[nt][ks], o[nt][dt], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  // Epilogue: lane holds row (l16) and head dims 16*dt + 4*lg + 0..3.
+  const int RBR = a.RB * kRowsPerBlock;
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt) {
+    float lt = l[nt];
+    lt += __shfl_xor(lt, 16, SRT_WAVE);
+    lt += __shfl_xor(lt, 32, SRT_WAVE);
+    if (!row_ok[nt]) continue;
+    const int r = rb * kRowsPerBlock + w * 32 + nt * 16 + l16;
+    if (nsplit == 1) {
+      const int h = g * a.G + r % a.G;
+      uint16_t* op = a.out + ((static_cast<int64_t>(b) * a.N + r / a.G) * a.Hq + h) * D + 4 * lg;
+      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+#pragma unroll
+      for (int dt = 0; dt < Sh::DT; ++dt) {
+        const uint32_t x0 = to_bf16_bits(o[nt][dt][0] * inv) | (uint32_t(to_bf16_bits(o[nt][dt][1] * inv)) << 16);
+        const uint32_t x1 = to_bf16_bits(o[nt][dt][2] * inv) | (uint32_t(to_bf16_bits(o[nt][dt][3] * inv)) << 16);
+        *reinterpret_cast<uint2*>(op + 16 * dt) = make_uint2(x0, x1);
+      }
+    } else {
+      const int64_t prow = ((static_cast<int64_t>(b) * a.Hkv + g) * a.S + s) * RBR + r;
+      float* po = a.part_o + prow * D + 4 * lg;
+#pragma unroll
+      for (int dt = 0; dt < Sh::DT; ++dt) *reinterpret_cast<f32x4*>(po + 16 * dt) = o[nt][dt];
+      if (lg == 0) {
+        a.part_ml[2 * prow] = m[nt];
+        a.part_ml[2 * prow + 1] = lt;
+      }
+    }
+  }
+}
+
+// Merges the split partials of sequences that needed more than one split.
+// One wave per output row (b, node, head).
+template <int D>
+__global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
+  const int wave = blockIdx.x * 4 + threadIdx.x / SRT_WAVE;
+  const int lane = threadIdx.x % SRT_WAVE;
+  const int per_seq = a.N * a.Hq;
+  if (wave >= a.B * per_seq) return;
+  const int b = wave / per_seq;
+  const int node = (wave % per_seq) / a.Hq;
+  const int h = wave % a.Hq;
+  const SeqInfo si = seq_info(a, b);
+  if (node >= si.n) return;
+  const int nsplit = (si.total + kChunk - 1) / kChunk;
+  if (nsplit <= 1) return;
+  const int g = h / a.G;
+  const int r = node * a.G + h % a.G;
+  const int RBR = a.RB * kRowsPerBlock;
+  const int64_t base = (static_cast<int64_t>(b) * a.Hkv + g) * a.S * RBR + r;
+  float M = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, a.part_ml[2 * (base + static_cast<int64_t>(s) * RBR)]);
+  constexpr int PER = D / SRT_WAVE;
+  float num[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) num[i] = 0.f;
+  float den = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const int64_t prow = base + static_cast<int64_t>(s) * RBR;
+    const float ms = a.part_ml[2 * prow];
+    const float wgt = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M);
+    den += wgt * a.part_ml[2 * prow + 1];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) num[i] += wgt * a.part_o[prow * D + lane + SRT_WAVE * i];
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  uint16_t* op = a.out + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + h) * D;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) op[lane + SRT_WAVE * i] = to_bf16_bits(num[i] * inv);
+}
+
+int splits_for(int32_t page, int32_t max_pages) {
+  const int64_t cap = static_cast<int64_t>(page) * max_pages;
+  return static_cast<int>((cap + kChunk - 1) / kChunk);
+}
+
+}  // namespace
+
+extern "C" size_t srt_tree_attn_scratch_bytes(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d, int32_t page,
+                                              int32_t max_pages) {
+  if (B < 0 || N < 1 || N > kMaxN || Hq < 1 || Hkv < 1 || Hq % Hkv || page < 1 || max_pages < 1) return 0;
+  const int S = splits_for(page, max_pages);
+  if (S <= 1) return 0;
+  const int G = Hq / Hkv;
+  const int64_t RBR = static_cast<int64_t>((N * G + kRowsPerBlock - 1) / kRowsPerBlock) * kRowsPerBlock;
+  return static_cast<size_t>(B) * Hkv * S * RBR * (d + 2) * sizeof(float);
+}
+
+extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d, int32_t page,
+                             int32_t max_pages, int64_t num_pages, const uint16_t* q, const uint16_t* k_cache,
+                             const uint16_t* v_cache, const int32_t* block_table, const int32_t* ctx_len,
+                             const int32_t* tree_parent, const int32_t* n_nodes, float scale, uint16_t* out,
+                             void* scratch, size_t scratch_bytes, void* stream) {
+  if (B < 0 || N < 1 || N > kMaxN || Hq < 1 || Hkv < 1 || Hq % Hkv || page < 1 || max_pages < 1 || num_pages < 1)
+    return SRT_ERR_INVALID;
+  if (!(scale == scale)) return SRT_ERR_INVALID;
+  if (d != 64 && d != 128) return SRT_ERR_UNSUPPORTED;
+  if (B == 0) return SRT_OK;
+  if (!q || !k_cache || !v_cache || !block_table || !ctx_len || !tree_parent || !n_nodes || !out)
+    return SRT_ERR_INVALID;
+  const size_t need = srt_tree_attn_scratch_bytes(B, N, Hq, Hkv, d, page, max_pages);
+  if (need > 0 && (!scratch || scratch_bytes < need)) return SRT_ERR_CAPACITY;
+
+  AttnArgs a;
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.bt = block_table;
+  a.ctx_len = ctx_len;
+  a.parent = tree_parent;
+  a.n_nodes = n_nodes;
+  a.out = out;
+  a.B = B;
+  a.N = N;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.G = Hq / Hkv;
+  a.page = page;
+  a.max_pages = max_pages;
+  a.num_pages = num_pages;
+  a.scale_log2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+  a.S = splits_for(page, max_pages);
+  a.RB = (N * a.G + kRowsPerBlock - 1) / kRowsPerBlock;
+  const int64_t total = static_cast<int64_t>(B) * Hkv * a.S * a.RB;
+  if (total > (int64_t(1) << 30)) return SRT_ERR_INVALID;
+  a.total = static_cast<int32_t>(total);
+  const int64_t RBR = static_cast<int64_t>(a.RB) * kRowsPerBlock;
+  a.part_o = static_cast<float*>(scratch);
+  a.part_ml = need ? static_cast<float*>(scratch) + static_cast<int64_t>(B) * Hkv * a.S * RBR * d : nullptr;
+
+  const unsigned grid = static_cast<unsigned>((total + kXcds - 1) / kXcds * kXcds);
+  hipStream_t s = as_stream(stream);
+  if (d == 128) {
+    tree_attn_kernel<128><<<grid, kThreads, 0, s>>>(a);
+  } else {
+    tree_attn_kernel<64><<<grid, kThreads, 0, s>>>(a);
+  }
+  if (a.S > 1) {
+    const int64_t rows = static_cast<int64_t>(B) * N * Hq;
+    const unsigned cgrid = static_cast<unsigned>((rows + 3) / 4);
+    if (d == 128) {
+      tree_attn_combine_kernel<128><<<cgrid, 256, 0, s>>>(a);
+    } else {
+      tree_attn_combine_kernel<64><<<cgrid, 256, 0, s>>>(a);
+    }
+  }
+  return launch_status();
+}

@@ -1,0 +1,90 @@
+"""The C-ABI library loads, exports every entry point include/srt.h declares,
+and rejects invalid arguments on the host before any HIP call (these tests
+run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2601_09083_amd import srt as S
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "srt.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(S.LIB_PATH), reason="libsrt.so not built")
+
+
+def declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(srt_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_binding_exports():
+    assert declared() == sorted(S.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = ctypes.CDLL(S.LIB_PATH)
+    for name in declared():
+        assert hasattr(L, name), name
+    assert S.srt_version().startswith("libsrt")
+
+
+def test_workspace_bytes_host_only():
+    assert S.srt_trie_workspace_bytes(4, 8, 12, 1000) > 0
+    assert S.srt_trie_workspace_bytes(0, 8, 12, 1000) == 0      # no prompts
+    assert S.srt_trie_workspace_bytes(4, 8, 65, 1000) == 0      # D > 64
+    assert S.srt_trie_workspace_bytes(4, 8, 12, 0) == 0         # no capacity
+    assert S.srt_trie_workspace_bytes(4, 8, 12, 1 << 40) == 0   # beyond 2^31 slots
+    a = S.srt_trie_workspace_bytes(4, 8, 12, 10_000)
+    b = S.srt_trie_workspace_bytes(4, 8, 12, 1_000_000)
+    assert b > a
+
+
+def test_scratch_bytes():
+    # one split: no scratch
+    assert S.srt_tree_attn_scratch_bytes(4, 8, 4, 1, 64, 16, 40) == 0
+    n = S.srt_tree_attn_scratch_bytes(256, 64, 28, 4, 128, 16, 2052)
+    assert n > 0 and n % 4 == 0
+    assert S.srt_tree_attn_scratch_bytes(4, 8, 5, 2, 64, 16, 40) == 0  # Hq % Hkv != 0
+
+
+def test_host_validation_before_any_hip_call():
+    L = S.lib()
+    cfg = S.TrieConfig(4, 8, 12, 0, 100)
+    assert L.srt_trie_init(None, 1 << 20, ctypes.byref(cfg), None) == S.SRT_ERR_INVALID
+    bad = S.TrieConfig(4, 8, 12, 1, 100)  # reserved != 0
+    assert L.srt_trie_init(ctypes.c_void_p(256), 1 << 20, ctypes.byref(bad), None) == S.SRT_ERR_INVALID
+    assert L.srt_trie_init(ctypes.c_void_p(255), 1 << 20, ctypes.byref(cfg), None) == S.SRT_ERR_INVALID  # alignment
+    assert L.srt_trie_init(ctypes.c_void_p(256), 64, ctypes.byref(cfg), None) == S.SRT_ERR_CAPACITY
+    assert L.srt_trie_insert(None, 1, None, None, None, None, 4, None) == S.SRT_ERR_INVALID
+    assert L.srt_trie_insert(ctypes.c_void_p(256), -1, None, None, None, None, 4, None) == S.SRT_ERR_INVALID
+    assert L.srt_trie_insert(ctypes.c_void_p(256), 0, None, None, None, None, 4, None) == S.SRT_OK  # no-op
+    assert L.srt_trie_reset_streams(ctypes.c_void_p(256), 0, None, None) == S.SRT_OK
+    assert L.srt_trie_status(None, None, None) == S.SRT_ERR_INVALID
+    p = S.DraftParams(8, 257, 4, 0, 0.0)   # N > 256
+    assert L.srt_draft(ctypes.c_void_p(256), 1, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
+    p = S.DraftParams(0, 8, 4, 0, 0.0)     # Qmax < 1
+    assert L.srt_draft(ctypes.c_void_p(256), 1, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
+    p = S.DraftParams(8, 8, 64, 0, 0.0)    # Dmax > 63
+    assert L.srt_draft(ctypes.c_void_p(256), 1, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
+    p = S.DraftParams(8, 8, 4, 0, 0.0)
+    assert L.srt_draft(ctypes.c_void_p(256), 0, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_OK  # B = 0
+    assert L.srt_draft(ctypes.c_void_p(256), 2, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
+    args = [4, 8, 4, 1, 96, 16, 40, 100] + [ctypes.c_void_p(256)] * 7 + [0.125, ctypes.c_void_p(256), None, 0, None]
+    assert L.srt_tree_attn(*args) == S.SRT_ERR_UNSUPPORTED           # d = 96
+    args[4] = 64; args[2] = 5; args[3] = 2
+    assert L.srt_tree_attn(*args) == S.SRT_ERR_INVALID               # Hq % Hkv
+    args[2] = 4; args[3] = 1; args[1] = 300
+    assert L.srt_tree_attn(*args) == S.SRT_ERR_INVALID               # N > 256
+    args[1] = 8; args[6] = 2052
+    assert L.srt_tree_attn(*args) == S.SRT_ERR_CAPACITY              # scratch needed, none given
+    acc = [4, 0, 16, 4, None, None, 1.0] + [None] * 7 + [None]
+    assert L.srt_accept(*acc) == S.SRT_ERR_INVALID                   # N = 0
+    acc[1] = 8; acc[3] = 64
+    assert L.srt_accept(*acc) == S.SRT_ERR_INVALID                   # Dmax > 63
+    acc[3] = 4
+    assert L.srt_accept(*acc) == S.SRT_ERR_INVALID                   # null pointers
+    acc[0] = 0
+    assert L.srt_accept(*acc) == S.SRT_OK                            # B = 0

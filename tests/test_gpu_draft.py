@@ -1,0 +1,87 @@
+"""GPU parity of srt_draft against the oracle draft, bit-exact: the tiny
+configuration, random small-vocabulary caches full of score ties, budget and
+depth variants, fallbacks, and a frontier overflow."""
+import random
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import draft as DR
+from oracle import trie as TR
+from paper_2601_09083_amd import srt
+from paper_2601_09083_amd import workload as W
+from paper_2601_09083_amd.pipeline import Caches, VerifyState
+from tests.gpu_util import assert_tree_equal, oracle_draft_rows, oracle_trie, say, tree_to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def run_draft(c, prompt_ids, tails, ts, Q, N, Dmax, alpha=0.0):
+    dev = "cuda"
+    t = lambda a: torch.as_tensor(np.asarray(a, dtype=np.int32), device=dev)
+    out = srt.srt_draft(c.ws, t(prompt_ids), t(tails), t(ts), Q, N, Dmax, alpha)
+    return tree_to_np(out)
+
+
+def test_tiny_config_exact():
+    cfg = W.CONFIGS["tiny"]
+    say("draft: tiny config")
+    st = VerifyState.build(cfg)
+    tree = tree_to_np(st.draft())
+    tries = [oracle_trie(st.tokens.streams_of_prompt(p), cfg.trie_depth) for p in range(cfg.n_prompts)]
+    want = oracle_draft_rows(st, tries, range(st.tokens.batch))
+    for b, w in want.items():
+        assert_tree_equal(tree, b, w)
+    assert (tree["n_nodes"] > 1).any()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_small_vocab_ties(seed):
+    rng = random.Random(seed)
+    P, B = 40, 120
+    D = rng.choice([4, 8, 12, 20])
+    vocab = rng.choice([2, 3, 5])
+    streams = [[np.array([rng.randrange(vocab) for _ in range(rng.randrange(1, 60))]) for _ in range(rng.randrange(1, 6))]
+               for _ in range(P)]
+    c = Caches.create(P, sum(len(s) for s in streams) + 1, D, 200000)
+    ids = c.new_streams(sum(len(s) for s in streams))
+    c.insert([p for p in range(P) for _ in streams[p]], ids, [x for s in streams for x in s])
+    tries = [TR.DictTrie(TR.substring_counts(streams[p], D), D) for p in range(P)]
+    Q = rng.randrange(1, min(D, 9))
+    for N, Dmax, alpha in [(rng.randrange(1, 40), rng.randrange(0, 10), 0.0), (256, 63, 0.0), (64, 12, 1.7)]:
+        say(f"draft: seed={seed} D={D} vocab={vocab} Q={Q} N={N} Dmax={Dmax} alpha={alpha}")
+        pids = [rng.randrange(P) for _ in range(B)]
+        tails = [[rng.randrange(vocab) for _ in range(Q)] for _ in range(B)]
+        ts = [rng.choice([0, 1, 2, Q, 100]) for _ in range(B)]
+        tree = run_draft(c, pids, tails, ts, Q, N, Dmax, alpha)
+        for b in range(B):
+            want = DR.draft(tries[pids[b]], tails[b][Q - min(ts[b], Q):] if ts[b] else [], ts[b], Q, N, Dmax, alpha)
+            assert_tree_equal(tree, b, want)
+
+
+def test_frontier_overflow_and_long_child_lists():
+    # node (7) has 1500 children of unequal counts: the frontier (512) must
+    # evict without losing any of the best 255 candidates
+    rng = np.random.default_rng(0)
+    D = 6
+    streams = [[np.array([7, int(x), int(y)]) for x, y in zip(rng.integers(0, 1500, size=4000),
+                                                               rng.integers(0, 3, size=4000))]]
+    c = Caches.create(1, 4001, D, 100000)
+    c.insert([0] * 4000, c.new_streams(4000), streams[0])
+    trie = TR.DictTrie(TR.substring_counts(streams[0], D), D)
+    for N, Dmax in [(256, 2), (256, 1), (100, 2)]:
+        say(f"draft: frontier overflow N={N} Dmax={Dmax}")
+        tree = run_draft(c, [0], [[7]], [5], 1, N, Dmax)
+        assert_tree_equal(tree, 0, DR.draft(trie, [7], 5, 1, N, Dmax))
+
+
+def test_deterministic_across_runs():
+    cfg = W.CONFIGS["tiny"].scaled(n_nodes=64, max_depth=12)
+    st = VerifyState.build(cfg)
+    say("draft: repeat determinism")
+    a = tree_to_np(st.draft())
+    for _ in range(3):
+        b = tree_to_np(st.draft())
+        for k in a:
+            assert np.array_equal(a[k], b[k])

@@ -1,0 +1,138 @@
+"""End-to-end parity of the verification step (draft -> tree attention ->
+acceptance -> online insertion) against the oracle.
+
+* tiny configuration: every sequence, two consecutive steps (the second
+  drafts from the cache updated by the first);
+* the four large configurations at full size, in the launch configuration
+  the benchmark times: the whole batch runs on the GPU and sampled sequences
+  (always including the longest context) are recomputed by the oracle one by
+  one; cache contents are checked exactly for a sampled prompt (or, for the
+  long-tail prompt, on sampled strings plus per-depth occurrence totals)."""
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import trie as TR
+from paper_2601_09083_amd import workload as W
+from paper_2601_09083_amd.pipeline import VerifyState
+from tests.gpu_util import (assert_accept_equal, assert_attn_close, assert_tree_equal, oracle_accept_rows,
+                            oracle_attention_seq, oracle_draft_rows, oracle_trie, say, tree_to_np)
+
+pytestmark = pytest.mark.gpu
+
+
+def overlay(tree_np, oracle_rows, N):
+    """Tree arrays with the oracle's rows written over the sampled sequences."""
+    t = {k: v.copy() for k, v in tree_np.items()}
+    for b, (tok, par, dep, n, q) in oracle_rows.items():
+        t["tree_tokens"][b] = -1; t["tree_parent"][b] = -1; t["tree_depth"][b] = -1
+        t["tree_tokens"][b, :n], t["tree_parent"][b, :n], t["tree_depth"][b, :n] = tok, par, dep
+        t["n_nodes"][b], t["match_len"][b] = n, q
+    return t
+
+
+def oracle_tree_arrays(rows, B, N):
+    t = {k: np.full((B, N), -1, np.int32) for k in ("tree_tokens", "tree_parent", "tree_depth")}
+    t["n_nodes"] = np.zeros(B, np.int32); t["match_len"] = np.zeros(B, np.int32)
+    return overlay(t, rows, N)
+
+
+@pytest.mark.parametrize("sampled", [False, True])
+def test_tiny_two_steps(sampled):
+    cfg = W.CONFIGS["tiny"]
+    st = VerifyState.build(cfg)
+    tw = st.tokens
+    B = tw.batch
+    streams = [list(tw.prior[p]) for p in range(cfg.n_prompts)]
+    seqs = [np.array(y) for y in tw.seqs]
+    for step in range(2):
+        say(f"step: tiny sampled={sampled} step={step}")
+        tries = [oracle_trie(streams[p] + [seqs[b] for b in range(B) if tw.seq_prompt[b] == p], cfg.trie_depth)
+                 for p in range(cfg.n_prompts)]
+        rows = oracle_draft_rows(st, tries, range(B))
+        tree = tree_to_np(st.draft())
+        for b in range(B):
+            assert_tree_equal(tree, b, rows[b])
+        ot = oracle_tree_arrays(rows, B, cfg.n_nodes)
+        st.logits = W.make_logits(cfg, ot["tree_tokens"], ot["tree_parent"], ot["n_nodes"], device="cuda",
+                                  boost="top", seed=100 + step)
+        st.gumbel = W.make_gumbel(cfg, B, device="cuda", seed=200 + step) if sampled else None
+        out = st.attention().float().cpu().numpy()
+        for b in range(B):
+            n = int(ot["n_nodes"][b])
+            assert_attn_close(out[b, :n], oracle_attention_seq(st, b, ot["tree_parent"][b], n), f"seq {b}")
+        acc = {k: v.cpu().numpy() for k, v in st.accept().items()}
+        want = oracle_accept_rows(st.logits, st.gumbel, 1.0, ot, range(B), cfg.max_depth)
+        for b in range(B):
+            assert_accept_equal(acc, b, want[b], cfg.max_depth)
+        st.insert()
+        for b in range(B):
+            seqs[b] = np.concatenate([seqs[b], np.array(want[b][1])])
+        for p in range(cfg.n_prompts):
+            allp = streams[p] + [seqs[b] for b in range(B) if tw.seq_prompt[b] == p]
+            assert st.caches.export(p) == TR.substring_counts(allp, cfg.trie_depth)
+    assert st.caches.status()["flags"] == 0
+
+
+FULL = {"qwen1.5b": 3, "grpo": 2, "qwen7b": 3, "longtail": 2}
+
+
+@pytest.mark.parametrize("name", list(FULL))
+def test_full_size_sampled(name):
+    cfg = W.CONFIGS[name]
+    say(f"full-size {name}: building caches, KV and queries")
+    st = VerifyState.build(cfg)
+    tw = st.tokens
+    B = tw.batch
+    rng = np.random.default_rng(cfg.index)
+    sample = sorted(set([int(np.argmax(tw.ctx_len))] + [int(x) for x in rng.choice(B, FULL[name], replace=False)]))
+    prompts = sorted(set(int(tw.seq_prompt[b]) for b in sample))
+    tries = {p: oracle_trie(tw.streams_of_prompt(p), cfg.trie_depth, big=True) for p in prompts}
+    say(f"full-size {name}: draft (sample {sample})")
+    tree = tree_to_np(st.draft())
+    rows = oracle_draft_rows(st, tries, sample)
+    for b in sample:
+        assert_tree_equal(tree, b, rows[b])
+    assert tree["n_nodes"].mean() > 2, "drafts should mostly succeed on this workload"
+    say(f"full-size {name}: attention")
+    out = st.attention()
+    torch.cuda.synchronize()
+    for b in sample:
+        n = int(rows[b][3])
+        ref = oracle_attention_seq(st, b, np.asarray(rows[b][1]), n)
+        assert_attn_close(out[b, :n].float().cpu().numpy(), ref, f"{name} seq {b}")
+    say(f"full-size {name}: acceptance (logits {B}x{cfg.n_nodes}x{cfg.vocab})")
+    t_in = overlay(tree, rows, cfg.n_nodes)
+    st.logits = W.make_logits(cfg, t_in["tree_tokens"], t_in["tree_parent"], t_in["n_nodes"], device="cuda")
+    st.gumbel = W.make_gumbel(cfg, B, device="cuda")
+    acc = {k: v.cpu().numpy() for k, v in st.accept().items()}
+    want = oracle_accept_rows(st.logits, st.gumbel, 1.0, t_in, sample, cfg.max_depth)
+    for b in sample:
+        assert_accept_equal(acc, b, want[b], cfg.max_depth)
+    say(f"full-size {name}: insertion")
+    st.insert()
+    if cfg.runahead_streams:
+        ids = st.caches.new_streams(B)
+        st.caches.insert(tw.seq_prompt, ids, tw.runahead)
+    assert st.caches.status()["flags"] == 0
+    p = prompts[0]
+    streams = list(tw.prior[p]) + [np.concatenate([tw.seqs[b], acc["out_tokens"][b, :acc["n_accepted"][b] + 1]])
+                                   for b in range(B) if tw.seq_prompt[b] == p]
+    if cfg.runahead_streams:
+        streams += [tw.runahead[b] for b in range(B) if tw.seq_prompt[b] == p]
+    got = st.caches.export(p)
+    D = cfg.trie_depth
+    if sum(len(s) for s in streams) * D < 3_000_000:
+        assert got == TR.substring_counts(streams, D)
+    else:
+        for ell in range(1, D + 1):  # per-depth occurrence totals
+            assert sum(c for s, c in got.items() if len(s) == ell) == sum(max(0, len(s) - ell + 1) for s in streams)
+        big = TR.StreamTrie(streams, D)
+        keys = list(got)
+        for i in rng.choice(len(keys), 300, replace=False):
+            assert got[keys[i]] == big.count(keys[i])
+    del st
+    gc.collect()
+    torch.cuda.empty_cache()

@@ -136,3 +136,18 @@ def test_pins_catch_planted_mistakes(golden_dir):
     assert _pins_pass(T.substring_counts, golden_dir)
     for bad in (_drop_last_level, _joined_streams, _set_semantics):
         assert not _pins_pass(bad, golden_dir), bad.__name__
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_online_insert_equals_definition(seed):
+    # appending chunk by chunk, streams interleaved, gives the batch map
+    rng = random.Random(500 + seed)
+    streams = rand_streams(rng, 4, 30, 3)
+    D = rng.randrange(1, 7)
+    counts, pos = {}, [0] * len(streams)
+    while any(p < len(s) for p, s in zip(pos, streams)):
+        i = rng.randrange(len(streams))
+        k = rng.randrange(0, 5)
+        T.insert_counts(counts, streams[i][:pos[i]], streams[i][pos[i]:pos[i] + k], D)
+        pos[i] += k
+    assert counts == T.substring_counts(streams, D)
