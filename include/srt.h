@@ -159,7 +159,8 @@ int srt_draft(const void* ws, int32_t B, const int32_t* prompt_ids, const int32_
  *   ctx_len, n_nodes [B] int32; tree_parent [B, N] int32 as from srt_draft.
  * Requirements: 1 <= n_nodes[b] <= N <= 256, parent[i] < i,
  *   L + n_nodes[b] <= max_pages * page, block_table entries < num_pages for
- *   the pages those positions use.  Values outside these ranges are clamped
+ *   the pages those positions use; page a power of two >= 16 (else
+ *   SRT_ERR_UNSUPPORTED).  Values outside these ranges are clamped
  *   or read as zero (never out of bounds); rows i >= n_nodes[b] of out are
  *   not written.  d must be 64 or 128; Hq % Hkv == 0.
  * scratch: device buffer of at least srt_tree_attn_scratch_bytes(...) bytes

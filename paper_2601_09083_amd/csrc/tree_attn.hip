@@ -60,7 +60,7 @@ struct AttnArgs {
   uint16_t* out;
   float* part_o;
   float* part_ml;
-  int32_t B, N, Hq, Hkv, G, page, max_pages;
+  int32_t B, N, Hq, Hkv, G, page, page_shift, max_pages;
   int64_t num_pages;
   float scale_log2;
   int32_t S, RB, total;
@@ -69,10 +69,9 @@ struct AttnArgs {
 template <int D>
 struct Shape {
   static constexpr int KS = D + 8;       // LDS row stride of the K tile (bf16 elements)
-  static constexpr int VS = kTile + 4;   // LDS row stride of the V^T tile
   static constexpr int KD = D / 32;      // MFMA steps over the head dimension
   static constexpr int DT = D / 16;      // 16-wide blocks of the head dimension
-  static constexpr int KCH = D / 32;     // 16-byte K chunks per thread per tile
+  static constexpr int KCH = D / 32;     // 16-byte chunks per thread per tile (K and V each)
 };
 
 __device__ inline uint16_t to_bf16_bits(float x) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x)); }
@@ -90,18 +89,18 @@ __device__ inline SeqInfo seq_info(const AttnArgs& a, int b) {
   return s;
 }
 
-// Element offset of position `pos` of KV head g of sequence b, or -1.
-__device__ inline int64_t kv_offset(const AttnArgs& a, int b, int g, int pos, int D) {
-  const int pg = a.bt[static_cast<int64_t>(b) * a.max_pages + pos / a.page];
-  if (pg < 0 || pg >= a.num_pages) return -1;
-  return ((static_cast<int64_t>(pg) * a.Hkv + g) * a.page + pos % a.page) * D;
+__device__ inline int sel4(int v0, int v1, int v2, int v3, int i) {
+  return i == 0 ? v0 : (i == 1 ? v1 : (i == 2 ? v2 : v3));
 }
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
   using Sh = Shape<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kTile * Sh::KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * Sh::VS];
+  constexpr int KS = Sh::KS;
+  constexpr int kTileElems = kTile * KS;
+  // Two LDS stages of K and V, both row-major [key][d] with a 16-byte pad.
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * kTileElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2 * kTileElems];
   __shared__ uint64_t anc[kMaxN][4];
   __shared__ int32_t spar[kMaxN];
 
@@ -129,6 +128,8 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
   const int lane = tid % SRT_WAVE;
   const int l16 = lane % 16;
   const int lg = lane / 16;
+  const int row0 = rb * kRowsPerBlock + w * 32;
+  const bool wave_active = row0 < rows;  // wave-uniform
 
   // Ancestor-or-self bitsets, needed only when this split reaches the tree.
   if (k_end > si.L) {
@@ -148,13 +149,13 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
     }
   }
 
-  // Query fragments: B operand of S^T = K Q^T (lane: row l16, head-dim 8*lg..+7).
+  // Query fragments: B operand of S^T = K Q^T (lane: row l16, head dims 8*lg..+7).
   bf16x8 qf[2][Sh::KD];
   int node_of[2];
   bool row_ok[2];
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt) {
-    const int r = rb * kRowsPerBlock + w * 32 + nt * 16 + l16;
+    const int r = row0 + nt * 16 + l16;
     row_ok[nt] = r < rows;
     const int node = row_ok[nt] ? r / a.G : 0;
     const int h = g * a.G + (row_ok[nt] ? r % a.G : 0);
@@ -162,13 +163,7 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
     const bf16x8* qp = reinterpret_cast<const bf16x8*>(
         a.q + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + h) * D + 8 * lg);
 #pragma unroll
-    for (int kd = 0; kd < Sh::KD; ++kd) {
-      if (row_ok[nt]) {
-        qf[nt][kd] = qp[4 * kd];
-      } else {
-        qf[nt][kd] = bf16x8{};
-      }
-    }
+    for (int kd = 0; kd < Sh::KD; ++kd) qf[nt][kd] = row_ok[nt] ? qp[4 * kd] : bf16x8{};
   }
 
   f32x4 o[2][Sh::DT];
@@ -176,164 +171,205 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
   for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
     for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // Reference maximum (log2 units) and lane-partial sums per row tile.  The
+  // reference is raised only when a row's maximum exceeds it by more than
+  // kLazy, so most tiles need no rescale of O.
+  constexpr float kLazy = 8.f;
   float m[2] = {-INFINITY, -INFINITY};
   float l[2] = {0.f, 0.f};
+  const float c = a.scale_log2;
 
-  // Staging assignment.  K: chunk c = tid + 256*i covers key c / (D/8), part c % (D/8).
-  // V: d-octet od = tid % (D/8), key quad kq = tid / (D/8) (keys 4kq..4kq+3).
-  uint4 kreg[Sh::KCH];
-  uint4 vreg[4];
+  // Staging: 16-byte chunk c = tid + 256*i of a [64][D] tile is key c/(D/8),
+  // part c%(D/8); K and V use the same assignment.  A tile is four 16-key
+  // sub-blocks, each inside one page (pages are powers of two >= 16); page
+  // ids are fetched one tile ahead of the data.
   constexpr int kOct = D / 8;
-  constexpr int kVThreads = kOct * (kTile / 4);  // 256 for D=128, 128 for D=64
-  const int od = tid % kOct;
-  const int kq = tid / kOct;
+  const int pshift = a.page_shift;
+  const int pmask = (1 << pshift) - 1;
+  const int64_t bt_row = static_cast<int64_t>(b) * a.max_pages;
+  const int32_t __attribute__((address_space(4)))* btc =
+      (const int32_t __attribute__((address_space(4)))*)(a.bt) + bt_row;
+  const int64_t head_stride = static_cast<int64_t>(a.page) * D;  // elements per (page, head)
 
-  auto load_tile = [&](int t0) {
+  auto tile_pages = [&](int t0, int* pg) {
 #pragma unroll
-    for (int i = 0; i < Sh::KCH; ++i) {
-      const int c = tid + kThreads * i;
-      const int key = c / kOct, part = c % kOct;
-      const int pos = t0 + key;
-      kreg[i] = make_uint4(0, 0, 0, 0);
-      if (pos < k_end) {
-        const int64_t off = kv_offset(a, b, g, pos, D);
-        if (off >= 0) kreg[i] = *reinterpret_cast<const uint4*>(a.k + off + part * 8);
-      }
-    }
-    if (tid < kVThreads) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int pos = t0 + 4 * kq + r;
-        vreg[r] = make_uint4(0, 0, 0, 0);
-        if (pos < k_end) {
-          const int64_t off = kv_offset(a, b, g, pos, D);
-          if (off >= 0) vreg[r] = *reinterpret_cast<const uint4*>(a.v + off + od * 8);
-        }
-      }
+    for (int i = 0; i < 4; ++i) {
+      const int p0 = t0 + 16 * i;
+      pg[i] = p0 < k_end ? btc[p0 >> pshift] : -1;
     }
   };
 
-  auto store_tile = [&]() {
+  uint4 kreg[Sh::KCH], vreg[Sh::KCH];
+  auto load_regs = [&](int t0, const int* pg_raw) {
+    int64_t base[4];
+    bool okp[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int pgi = pg_raw[i];
+      okp[i] = pgi >= 0 && pgi < a.num_pages;
+      // element offset of slot 0 of this sub-block within the cache
+      base[i] = okp[i] ? (static_cast<int64_t>(pgi) * a.Hkv + g) * head_stride + ((t0 + 16 * i) & pmask) * D : 0;
+    }
+    const bool full = (t0 + kTile <= k_end) && okp[0] && okp[1] && okp[2] && okp[3];
 #pragma unroll
     for (int i = 0; i < Sh::KCH; ++i) {
-      const int c = tid + kThreads * i;
-      const int key = c / kOct, part = c % kOct;
-      *reinterpret_cast<uint4*>(&Ks[key * Sh::KS + part * 8]) = kreg[i];
-    }
-    if (tid < kVThreads) {
-      // 4 keys x 8 dims -> 8 rows of V^T, 4 keys each.
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int sh = (e & 1) * 16;
-        const uint32_t a0 = (w0[e >> 1] >> sh) & 0xFFFFu, a1 = (w1[e >> 1] >> sh) & 0xFFFFu;
-        const uint32_t a2 = (w2[e >> 1] >> sh) & 0xFFFFu, a3 = (w3[e >> 1] >> sh) & 0xFFFFu;
-        *reinterpret_cast<uint2*>(&Vt[(8 * od + e) * Sh::VS + 4 * kq]) = make_uint2(a0 | (a1 << 16), a2 | (a3 << 16));
+      const int cidx = tid + kThreads * i;
+      const int key = cidx / kOct, part = cidx % kOct;
+      const int sb = key >> 4;
+      const int64_t bsel = sb == 0 ? base[0] : (sb == 1 ? base[1] : (sb == 2 ? base[2] : base[3]));
+      const int64_t off = bsel + (key & 15) * D + part * 8;
+      if (full) {
+        kreg[i] = *reinterpret_cast<const uint4*>(a.k + off);
+        vreg[i] = *reinterpret_cast<const uint4*>(a.v + off);
+      } else {
+        const bool oksb = sb == 0 ? okp[0] : (sb == 1 ? okp[1] : (sb == 2 ? okp[2] : okp[3]));
+        const bool ok = oksb && (t0 + key < k_end);
+        const int64_t o2 = ok ? off : 0;
+        const uint4 xk = *reinterpret_cast<const uint4*>(a.k + o2);
+        const uint4 xv = *reinterpret_cast<const uint4*>(a.v + o2);
+        kreg[i] = ok ? xk : make_uint4(0, 0, 0, 0);
+        vreg[i] = ok ? xv : make_uint4(0, 0, 0, 0);
       }
     }
   };
+  auto store_regs = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < Sh::KCH; ++i) {
+      const int cidx = tid + kThreads * i;
+      const int key = cidx / kOct, part = cidx % kOct;
+      *reinterpret_cast<uint4*>(&Ks[buf * kTileElems + key * KS + part * 8]) = kreg[i];
+      *reinterpret_cast<uint4*>(&Vs[buf * kTileElems + key * KS + part * 8]) = vreg[i];
+    }
+  };
+
+  // Per-lane LDS offsets (elements) of the MFMA operand reads.
+  const int k_rd = l16 * KS + 8 * lg;                               // + 16*mt*KS + 32*kd
+  const int v_rd = (4 * lg + l16 / 4) * KS + 4 * (l16 % 4);         // + 32*ks*KS (+16*KS) + 16*dt
 
   const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
-  load_tile(k_begin);
+  int pg[4];
+  tile_pages(k_begin, pg);
+  load_regs(k_begin, pg);
+  store_regs(0);
+  if (ntiles > 1) {
+    tile_pages(k_begin + kTile, pg);
+    load_regs(k_begin + kTile, pg);
+  }
+  tile_pages(k_begin + 2 * kTile, pg);
+  __syncthreads();
+
   for (int it = 0; it < ntiles; ++it) {
     const int t0 = k_begin + it * kTile;
-    store_tile();
-    __syncthreads();
-    if (it + 1 < ntiles) load_tile(t0 + kTile);
-
-    // S^T[key][row] for 4 key groups x 2 row tiles.
-    f32x4 sacc[2][4];
+    const int buf = it & 1;
+    if (wave_active) {
+      const uint16_t* Kb = Ks + buf * kTileElems;
+      const uint16_t* Vb = Vs + buf * kTileElems;
+      // S^T[key][row] for 4 key groups x 2 row tiles.
+      f32x4 sacc[2][4];
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
+      for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) sacc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int mt = 0; mt < 4; ++mt) sacc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kd = 0; kd < Sh::KD; ++kd) {
+      for (int kd = 0; kd < Sh::KD; ++kd) {
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&Ks[(16 * mt + l16) * Sh::KS + 32 * kd + 8 * lg]);
+        for (int mt = 0; mt < 4; ++mt) {
+          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Kb + k_rd + 16 * mt * KS + 32 * kd);
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          sacc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[nt][kd], sacc[nt][mt], 0, 0, 0);
+          for (int nt = 0; nt < 2; ++nt)
+            sacc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[nt][kd], sacc[nt][mt], 0, 0, 0);
+        }
       }
-    }
 
-    // Mask, online softmax, P in bf16.
-    const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
-    bf16x8 pb[2][2];
+      // Mask, online softmax with lazy rescale, P in bf16.
+      const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
+      bf16x8 pb[2][2];
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      float mloc = -INFINITY;
+      for (int nt = 0; nt < 2; ++nt) {
+        if (need_mask) {
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
+          for (int mt = 0; mt < 4; ++mt) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float x = sacc[nt][mt][r] * a.scale_log2;
-          if (need_mask) {
-            const int pos = t0 + 16 * mt + 4 * lg + r;
-            bool vis = pos < k_end;
-            if (vis && pos >= si.L) {
-              const int j = pos - si.L;
-              vis = (anc[node_of[nt]][j >> 6] >> (j & 63)) & 1ull;
+            for (int r = 0; r < 4; ++r) {
+              const int pos = t0 + 16 * mt + 4 * lg + r;
+              bool vis = pos < k_end;
+              if (vis && pos >= si.L) {
+                const int j = pos - si.L;
+                vis = (anc[node_of[nt]][j >> 6] >> (j & 63)) & 1ull;
+              }
+              if (!vis) sacc[nt][mt][r] = -INFINITY;
             }
-            if (!vis) x = -INFINITY;
           }
-          sacc[nt][mt][r] = x;
-          mloc = fmaxf(mloc, x);
+        }
+        float mloc = fmaxf(fmaxf(sacc[nt][0][0], sacc[nt][0][1]), fmaxf(sacc[nt][0][2], sacc[nt][0][3]));
+#pragma unroll
+        for (int mt = 1; mt < 4; ++mt)
+          mloc = fmaxf(mloc, fmaxf(fmaxf(sacc[nt][mt][0], sacc[nt][mt][1]), fmaxf(sacc[nt][mt][2], sacc[nt][mt][3])));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, SRT_WAVE));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, SRT_WAVE));
+        const float ms = mloc * c;  // row max in log2 units (c > 0)
+        const bool raise = ms > m[nt] + kLazy;
+        if (__ballot(raise)) {
+          const float mnew = raise ? ms : m[nt];
+          const float alpha = m[nt] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
+          l[nt] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] *= alpha;
+          m[nt] = mnew;
+        }
+        const float mref = m[nt] == -INFINITY ? 0.f : m[nt];
+        float psum = 0.f;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[nt][mt][r], c, -mref));
+            sacc[nt][mt][r] = p;
+            psum += p;
+          }
+        }
+        l[nt] += psum;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            pb[nt][ks][r] = static_cast<__bf16>(sacc[nt][2 * ks][r]);
+            pb[nt][ks][4 + r] = static_cast<__bf16>(sacc[nt][2 * ks + 1][r]);
+          }
         }
       }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, SRT_WAVE));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, SRT_WAVE));
-      const float mnew = fmaxf(m[nt], mloc);
-      const bool dead = mnew == -INFINITY;
-      const float alpha = dead ? 1.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
-      float psum = 0.f;
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = dead ? 0.f : __builtin_amdgcn_exp2f(sacc[nt][mt][r] - mnew);
-          sacc[nt][mt][r] = p;
-          psum += p;
-        }
-      }
-      l[nt] = l[nt] * alpha + psum;
-      m[nt] = mnew;
-#pragma unroll
-      for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] *= alpha;
+
+      // O^T[d][row] += V^T P^T.  Contraction index (8*lg + e) <-> key
+      // 32*ks + 16*(e/4) + 4*lg + e%4, matching the S^T layout; the V^T
+      // operand comes from transposing LDS reads of the row-major V tile.
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          pb[nt][ks][r] = static_cast<__bf16>(sacc[nt][2 * ks][r]);
-          pb[nt][ks][4 + r] = static_cast<__bf16>(sacc[nt][2 * ks + 1][r]);
+        for (int dt = 0; dt < Sh::DT; ++dt) {
+          typedef short i16x4 __attribute__((ext_vector_type(4)));
+          const uint16_t* vp = Vb + v_rd + 32 * ks * KS + 16 * dt;
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) i16x4*)(vp));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) i16x4*)(vp + 16 * KS));
+          typedef short i16x8 __attribute__((ext_vector_type(8)));
+          const i16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          const bf16x8 va = __builtin_bit_cast(bf16x8, both);
+#pragma unroll
+          for (int nt = 0; nt < 2; ++nt)
+            o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[nt][ks], o[nt][dt], 0, 0, 0);
         }
       }
     }
-
-    // O^T[d][row] += V^T P^T; contraction index (8*lg + e) <-> key
-    // 32*ks + 16*(e/4) + 4*lg + e%4, matching the S^T output layout.
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-      for (int dt = 0; dt < Sh::DT; ++dt) {
-        const uint16_t* vp = &Vt[(16 * dt + l16) * Sh::VS + 32 * ks + 4 * lg];
-        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 16);
-        const uint4 packed = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        const bf16x8 va = __builtin_bit_cast(bf16x8, packed);
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[nt][ks], o[nt][dt], 0, 0, 0);
-      }
+    if (it + 1 < ntiles) store_regs(buf ^ 1);
+    if (it + 2 < ntiles) {
+      load_regs(t0 + 2 * kTile, pg);
+      tile_pages(t0 + 3 * kTile, pg);
     }
     __syncthreads();
   }
 
-  // Epilogue: lane holds row (l16) and head dims 16*dt + 4*lg + 0..3.
+  // Epilogue: lane holds row l16 and head dims 16*dt + 4*lg + 0..3.
   const int RBR = a.RB * kRowsPerBlock;
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt) {
@@ -341,7 +377,7 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
     lt += __shfl_xor(lt, 16, SRT_WAVE);
     lt += __shfl_xor(lt, 32, SRT_WAVE);
     if (!row_ok[nt]) continue;
-    const int r = rb * kRowsPerBlock + w * 32 + nt * 16 + l16;
+    const int r = row0 + nt * 16 + l16;
     if (nsplit == 1) {
       const int h = g * a.G + r % a.G;
       uint16_t* op = a.out + ((static_cast<int64_t>(b) * a.N + r / a.G) * a.Hq + h) * D + 4 * lg;
@@ -431,6 +467,7 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
     return SRT_ERR_INVALID;
   if (!(scale == scale)) return SRT_ERR_INVALID;
   if (d != 64 && d != 128) return SRT_ERR_UNSUPPORTED;
+  if (page < 16 || (page & (page - 1))) return SRT_ERR_UNSUPPORTED;
   if (B == 0) return SRT_OK;
   if (!q || !k_cache || !v_cache || !block_table || !ctx_len || !tree_parent || !n_nodes || !out)
     return SRT_ERR_INVALID;
@@ -452,6 +489,7 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
   a.Hkv = Hkv;
   a.G = Hq / Hkv;
   a.page = page;
+  a.page_shift = __builtin_ctz(static_cast<unsigned>(page));
   a.max_pages = max_pages;
   a.num_pages = num_pages;
   a.scale_log2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);

@@ -119,9 +119,10 @@ CONFIGS = {
                    ctx_len=Dist("lognormal", 2048, 16384), n_nodes=64, max_depth=12,
                    hq=12, hkv=2, head_dim=128),
     # Qwen2.5-7B-shaped attention layer, 256 sequences, log-normal contexts
-    # (median 4k, max 32k).
+    # (median 4k, max 32k); prior rollouts are log-normal like the contexts,
+    # so the caches cover the positions being drafted.
     "qwen7b": Config("qwen7b", 3, n_prompts=256, seqs_per_prompt=1, vocab=152064,
-                     rollouts_per_prompt=16, rollout_len=Dist("uniform", 1024, 4096),
+                     rollouts_per_prompt=16, rollout_len=Dist("lognormal", 4096, 32768),
                      ctx_len=Dist("lognormal", 4096, 32768), n_nodes=64, max_depth=12,
                      hq=28, hkv=4, head_dim=128),
     # Long-tail run-ahead regime: 8 sequences of 16k-32k, 256-node trees,
