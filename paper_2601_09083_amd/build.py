@@ -36,6 +36,13 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError("hipcc failed building libsrt.so")
+    # every symbol must resolve (a kernel whose host stub the host pass failed
+    # to emit shows up here as an undefined symbol)
+    chk = subprocess.run([sys.executable, "-c", "import ctypes, sys; ctypes.CDLL(sys.argv[1], mode=2)",
+                          LIB + ".tmp"], capture_output=True, text=True)
+    if chk.returncode != 0:
+        sys.stderr.write(chk.stderr)
+        raise RuntimeError("libsrt.so built but does not load")
     os.replace(LIB + ".tmp", LIB)
     return LIB
 

@@ -31,6 +31,7 @@
 //   * Block ids are remapped so that the row blocks and splits of one
 //     (sequence, KV head) run on the same XCD and share its L2.
 #include <cmath>
+#include <type_traits>
 
 #include "common.h"
 
@@ -68,10 +69,8 @@ struct AttnArgs {
 
 template <int D>
 struct Shape {
-  static constexpr int KS = D + 8;       // LDS row stride of the K tile (bf16 elements)
   static constexpr int KD = D / 32;      // MFMA steps over the head dimension
   static constexpr int DT = D / 16;      // 16-wide blocks of the head dimension
-  static constexpr int KCH = D / 32;     // 16-byte chunks per thread per tile (K and V each)
 };
 
 __device__ inline uint16_t to_bf16_bits(float x) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x)); }
@@ -89,16 +88,27 @@ __device__ inline SeqInfo seq_info(const AttnArgs& a, int b) {
   return s;
 }
 
-__device__ inline int sel4(int v0, int v1, int v2, int v3, int i) {
-  return i == 0 ? v0 : (i == 1 ? v1 : (i == 2 ? v2 : v3));
+// Loads kLoads x 1 KB from `base` (nbytes valid, the rest reads as zero)
+// straight into LDS: load j writes lds + j*stride_elems, lane l's 16 bytes
+// (from byte offset voff[j]) at offset 16*l.
+template <int kLoads>
+__device__ inline void buffer_to_lds(const uint16_t* base, int nbytes, uint16_t* lds, int stride_elems,
+                                     const int (&voff)[kLoads]) {
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, nbytes, 0x00020000);
+#pragma unroll
+  for (int j = 0; j < kLoads; ++j)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(lds + j * stride_elems),
+                                             16, voff[j], 0, 0, 0);
 }
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
   using Sh = Shape<D>;
-  constexpr int KS = Sh::KS;
-  constexpr int kTileElems = kTile * KS;
-  // Two LDS stages of K and V, both row-major [key][d] with a 16-byte pad.
+  constexpr int CPR = D / 8;                 // 16-byte chunks per K/V row
+  constexpr int kTileElems = kTile * D;      // unpadded, chunk-swizzled rows
+  // K is consumed one tile before V (pipelining below), so each has its own
+  // pair of LDS buffers.
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * kTileElems];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2 * kTileElems];
   __shared__ uint64_t anc[kMaxN][4];
@@ -124,7 +134,7 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
   const int nsplit = (si.total + kChunk - 1) / kChunk;
 
   const int tid = threadIdx.x;
-  const int w = tid / SRT_WAVE;
+  const int w = __builtin_amdgcn_readfirstlane(tid / SRT_WAVE);  // wave-uniform, in an SGPR
   const int lane = tid % SRT_WAVE;
   const int l16 = lane % 16;
   const int lg = lane / 16;
@@ -179,194 +189,212 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
   float l[2] = {0.f, 0.f};
   const float c = a.scale_log2;
 
-  // Staging: 16-byte chunk c = tid + 256*i of a [64][D] tile is key c/(D/8),
-  // part c%(D/8); K and V use the same assignment.  A tile is four 16-key
-  // sub-blocks, each inside one page (pages are powers of two >= 16); page
-  // ids are fetched one tile ahead of the data.
-  constexpr int kOct = D / 8;
+  // ---- staging ----------------------------------------------------------
+  // K and V tiles go straight from HBM to LDS (buffer loads with the LDS
+  // destination; no staging registers).  Wave w moves the w-th 16-key
+  // sub-block of a tile, which lies inside one page (pages are powers of two
+  // >= 16): one buffer descriptor covers exactly its valid keys, so keys past
+  // the split end or on an invalid page read as zero.  Row r's 16-byte chunk
+  // c is stored at chunk position c ^ (r % CPR) (conflict-free operand reads);
+  // a load instruction writes 1 KB contiguous, lane l at offset 16*l, so lane
+  // l fetches the chunk that belongs at its position.
   const int pshift = a.page_shift;
   const int pmask = (1 << pshift) - 1;
   const int64_t bt_row = static_cast<int64_t>(b) * a.max_pages;
   const int32_t __attribute__((address_space(4)))* btc =
       (const int32_t __attribute__((address_space(4)))*)(a.bt) + bt_row;
   const int64_t head_stride = static_cast<int64_t>(a.page) * D;  // elements per (page, head)
-
-  auto tile_pages = [&](int t0, int* pg) {
+  constexpr int kRowsPerLoad = 1024 / (2 * D);                    // 4 (d=128) or 8 (d=64)
+  constexpr int kLoadsPerWave = 16 / kRowsPerLoad;                // per tile, per tensor
+  // Per-lane byte offset inside the sub-block and LDS placement of each load.
+  int lane_voff[kLoadsPerWave];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int p0 = t0 + 16 * i;
-      pg[i] = p0 < k_end ? btc[p0 >> pshift] : -1;
-    }
-  };
-
-  uint4 kreg[Sh::KCH], vreg[Sh::KCH];
-  auto load_regs = [&](int t0, const int* pg_raw) {
-    int64_t base[4];
-    bool okp[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int pgi = pg_raw[i];
-      okp[i] = pgi >= 0 && pgi < a.num_pages;
-      // element offset of slot 0 of this sub-block within the cache
-      base[i] = okp[i] ? (static_cast<int64_t>(pgi) * a.Hkv + g) * head_stride + ((t0 + 16 * i) & pmask) * D : 0;
-    }
-    const bool full = (t0 + kTile <= k_end) && okp[0] && okp[1] && okp[2] && okp[3];
-#pragma unroll
-    for (int i = 0; i < Sh::KCH; ++i) {
-      const int cidx = tid + kThreads * i;
-      const int key = cidx / kOct, part = cidx % kOct;
-      const int sb = key >> 4;
-      const int64_t bsel = sb == 0 ? base[0] : (sb == 1 ? base[1] : (sb == 2 ? base[2] : base[3]));
-      const int64_t off = bsel + (key & 15) * D + part * 8;
-      if (full) {
-        kreg[i] = *reinterpret_cast<const uint4*>(a.k + off);
-        vreg[i] = *reinterpret_cast<const uint4*>(a.v + off);
-      } else {
-        const bool oksb = sb == 0 ? okp[0] : (sb == 1 ? okp[1] : (sb == 2 ? okp[2] : okp[3]));
-        const bool ok = oksb && (t0 + key < k_end);
-        const int64_t o2 = ok ? off : 0;
-        const uint4 xk = *reinterpret_cast<const uint4*>(a.k + o2);
-        const uint4 xv = *reinterpret_cast<const uint4*>(a.v + o2);
-        kreg[i] = ok ? xk : make_uint4(0, 0, 0, 0);
-        vreg[i] = ok ? xv : make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto store_regs = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < Sh::KCH; ++i) {
-      const int cidx = tid + kThreads * i;
-      const int key = cidx / kOct, part = cidx % kOct;
-      *reinterpret_cast<uint4*>(&Ks[buf * kTileElems + key * KS + part * 8]) = kreg[i];
-      *reinterpret_cast<uint4*>(&Vs[buf * kTileElems + key * KS + part * 8]) = vreg[i];
-    }
-  };
-
-  // Per-lane LDS offsets (elements) of the MFMA operand reads.
-  const int k_rd = l16 * KS + 8 * lg;                               // + 16*mt*KS + 32*kd
-  const int v_rd = (4 * lg + l16 / 4) * KS + 4 * (l16 % 4);         // + 32*ks*KS (+16*KS) + 16*dt
-
-  const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
-  int pg[4];
-  tile_pages(k_begin, pg);
-  load_regs(k_begin, pg);
-  store_regs(0);
-  if (ntiles > 1) {
-    tile_pages(k_begin + kTile, pg);
-    load_regs(k_begin + kTile, pg);
+  for (int j = 0; j < kLoadsPerWave; ++j) {
+    const int r = kRowsPerLoad * j + lane / CPR;     // row within the sub-block (0..15)
+    const int pos = lane % CPR;                      // chunk position written by this lane
+    const int row = 16 * w + r;                      // row within the tile
+    const int chunk = pos ^ (row & (CPR - 1));
+    lane_voff[j] = (r * D + chunk * 8) * 2;
   }
-  tile_pages(k_begin + 2 * kTile, pg);
-  __syncthreads();
 
-  for (int it = 0; it < ntiles; ++it) {
-    const int t0 = k_begin + it * kTile;
-    const int buf = it & 1;
-    if (wave_active) {
-      const uint16_t* Kb = Ks + buf * kTileElems;
-      const uint16_t* Vb = Vs + buf * kTileElems;
-      // S^T[key][row] for 4 key groups x 2 row tiles.
-      f32x4 sacc[2][4];
+  // Page id of this wave's sub-block of the tile at t0 (-1 if none).
+  auto sub_page = [&](int t0) {
+    const int p0 = t0 + 16 * w;
+    return p0 < k_end ? btc[p0 >> pshift] : -1;
+  };
+  auto issue_tile = [&](const uint16_t* src, uint16_t* dst, int t0, int pg) {
+    const int p0 = t0 + 16 * w;
+    const bool ok = pg >= 0 && pg < a.num_pages && p0 < k_end;
+    const int nkeys = ok ? min(16, k_end - p0) : 0;
+    const uint16_t* base = ok ? src + (static_cast<int64_t>(pg) * a.Hkv + g) * head_stride + (p0 & pmask) * D : src;
+    buffer_to_lds<kLoadsPerWave>(base, nkeys * D * 2, dst + 16 * w * D, kRowsPerLoad * D, lane_voff);
+  };
+
+  // ---- MFMA phases -------------------------------------------------------
+  // Lane offsets (elements) of the swizzled operand reads.  For K the XOR
+  // term depends only on the lane's row within a 16-row group, so row groups
+  // (mt) add a constant; for V it depends on the row within 16 as well, so
+  // ks and the +16-row half add constants.  Only the head-dim index varies
+  // non-linearly and gets its own register.
+  int koff[Sh::KD];
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
+  for (int kd = 0; kd < Sh::KD; ++kd) koff[kd] = (l16 * CPR + ((4 * kd + lg) ^ (l16 & (CPR - 1)))) * 8;
+  int voff[Sh::DT];
+  {
+    const int r0 = 4 * lg + l16 / 4;  // row within the 32-row group, < 16
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) sacc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int dt = 0; dt < Sh::DT; ++dt)
+      voff[dt] = (r0 * CPR + ((2 * dt + ((l16 & 3) >> 1)) ^ (r0 & (CPR - 1)))) * 8 + (l16 & 1) * 4;
+  }
+
+  // S^T[key][row] of one tile: 4 key groups x 2 row tiles.
+  auto qk = [&](const uint16_t* Kb, f32x4 (&sacc)[2][4]) {
 #pragma unroll
-      for (int kd = 0; kd < Sh::KD; ++kd) {
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) sacc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kd = 0; kd < Sh::KD; ++kd) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Kb + 16 * mt * D + koff[kd]);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+          sacc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[nt][kd], sacc[nt][mt], 0, 0, 0);
+      }
+    }
+  };
+
+  // Mask, online softmax with lazy rescale; returns P in bf16.
+  auto softmax = [&](int t0, f32x4 (&sacc)[2][4], bf16x8 (&pb)[2][2]) {
+    const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      if (need_mask) {
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
-          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Kb + k_rd + 16 * mt * KS + 32 * kd);
+          f32x4 t = sacc[nt][mt];
 #pragma unroll
-          for (int nt = 0; nt < 2; ++nt)
-            sacc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[nt][kd], sacc[nt][mt], 0, 0, 0);
-        }
-      }
-
-      // Mask, online softmax with lazy rescale, P in bf16.
-      const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
-      bf16x8 pb[2][2];
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        if (need_mask) {
-#pragma unroll
-          for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int pos = t0 + 16 * mt + 4 * lg + r;
-              bool vis = pos < k_end;
-              if (vis && pos >= si.L) {
-                const int j = pos - si.L;
-                vis = (anc[node_of[nt]][j >> 6] >> (j & 63)) & 1ull;
-              }
-              if (!vis) sacc[nt][mt][r] = -INFINITY;
+          for (int r = 0; r < 4; ++r) {
+            const int pos = t0 + 16 * mt + 4 * lg + r;
+            bool vis = pos < k_end;
+            if (vis && pos >= si.L) {
+              const int j = pos - si.L;
+              vis = (anc[node_of[nt]][j >> 6] >> (j & 63)) & 1ull;
             }
+            t[r] = vis ? t[r] : -INFINITY;
           }
-        }
-        float mloc = fmaxf(fmaxf(sacc[nt][0][0], sacc[nt][0][1]), fmaxf(sacc[nt][0][2], sacc[nt][0][3]));
-#pragma unroll
-        for (int mt = 1; mt < 4; ++mt)
-          mloc = fmaxf(mloc, fmaxf(fmaxf(sacc[nt][mt][0], sacc[nt][mt][1]), fmaxf(sacc[nt][mt][2], sacc[nt][mt][3])));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, SRT_WAVE));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, SRT_WAVE));
-        const float ms = mloc * c;  // row max in log2 units (c > 0)
-        const bool raise = ms > m[nt] + kLazy;
-        if (__ballot(raise)) {
-          const float mnew = raise ? ms : m[nt];
-          const float alpha = m[nt] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
-          l[nt] *= alpha;
-#pragma unroll
-          for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] *= alpha;
-          m[nt] = mnew;
-        }
-        const float mref = m[nt] == -INFINITY ? 0.f : m[nt];
-        float psum = 0.f;
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[nt][mt][r], c, -mref));
-            sacc[nt][mt][r] = p;
-            psum += p;
-          }
-        }
-        l[nt] += psum;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            pb[nt][ks][r] = static_cast<__bf16>(sacc[nt][2 * ks][r]);
-            pb[nt][ks][4 + r] = static_cast<__bf16>(sacc[nt][2 * ks + 1][r]);
-          }
+          sacc[nt][mt] = t;
         }
       }
-
-      // O^T[d][row] += V^T P^T.  Contraction index (8*lg + e) <-> key
-      // 32*ks + 16*(e/4) + 4*lg + e%4, matching the S^T layout; the V^T
-      // operand comes from transposing LDS reads of the row-major V tile.
+      float mloc = fmaxf(fmaxf(sacc[nt][0][0], sacc[nt][0][1]), fmaxf(sacc[nt][0][2], sacc[nt][0][3]));
+#pragma unroll
+      for (int mt = 1; mt < 4; ++mt)
+        mloc = fmaxf(mloc, fmaxf(fmaxf(sacc[nt][mt][0], sacc[nt][mt][1]), fmaxf(sacc[nt][mt][2], sacc[nt][mt][3])));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, SRT_WAVE));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, SRT_WAVE));
+      const float ms = mloc * c;  // row max in log2 units (c > 0)
+      const bool raise = ms > m[nt] + kLazy;
+      if (__ballot(raise)) {
+        const float mnew = raise ? ms : m[nt];
+        const float alpha = m[nt] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
+        l[nt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] *= alpha;
+        m[nt] = mnew;
+      }
+      const float mref = m[nt] == -INFINITY ? 0.f : m[nt];
+      float psum = 0.f;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[nt][mt][r], c, -mref));
+          sacc[nt][mt][r] = p;
+          psum += p;
+        }
+      }
+      l[nt] += psum;
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-        for (int dt = 0; dt < Sh::DT; ++dt) {
-          typedef short i16x4 __attribute__((ext_vector_type(4)));
-          const uint16_t* vp = Vb + v_rd + 32 * ks * KS + 16 * dt;
-          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) i16x4*)(vp));
-          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) i16x4*)(vp + 16 * KS));
-          typedef short i16x8 __attribute__((ext_vector_type(8)));
-          const i16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          const bf16x8 va = __builtin_bit_cast(bf16x8, both);
-#pragma unroll
-          for (int nt = 0; nt < 2; ++nt)
-            o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[nt][ks], o[nt][dt], 0, 0, 0);
+        for (int r = 0; r < 4; ++r) {
+          pb[nt][ks][r] = static_cast<__bf16>(sacc[nt][2 * ks][r]);
+          pb[nt][ks][4 + r] = static_cast<__bf16>(sacc[nt][2 * ks + 1][r]);
         }
       }
     }
-    if (it + 1 < ntiles) store_regs(buf ^ 1);
-    if (it + 2 < ntiles) {
-      load_regs(t0 + 2 * kTile, pg);
-      tile_pages(t0 + 3 * kTile, pg);
+  };
+
+  // O^T[d][row] += V^T P^T.  Contraction index (8*lg + e) <-> key
+  // 32*ks + 16*(e/4) + 4*lg + e%4, matching the S^T layout; the V^T operand
+  // comes from transposing LDS reads: lane (lg, l16) addresses row
+  // 32*ks + 4*lg + l16/4 (+16), head dims 16*dt + 4*(l16%4) .. +3.
+  auto pv = [&](const uint16_t* Vb, const bf16x8 (&pb)[2][2]) {
+    typedef short i16x4 __attribute__((ext_vector_type(4)));
+    typedef short i16x8 __attribute__((ext_vector_type(8)));
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+      for (int dt = 0; dt < Sh::DT; ++dt) {
+        const uint16_t* p0 = Vb + 32 * ks * D + voff[dt];
+        const uint16_t* p1 = p0 + 16 * D;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p1));
+        const i16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        const bf16x8 va = __builtin_bit_cast(bf16x8, both);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+          o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[nt][ks], o[nt][dt], 0, 0, 0);
+      }
     }
+  };
+
+  // ---- software pipeline -------------------------------------------------
+  // Iteration t: global loads of K(t+2) and V(t+1) are issued; S(t+1) = K Q^T
+  // of the next tile runs on the MFMA pipe while softmax(t) runs on the VALU;
+  // then O += V(t)^T P(t); finally K(t+2) and V(t+1) go to the buffers that
+  // K(t) and V(t-1) have left.  One barrier per tile.
+  const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
+  int pgA = sub_page(k_begin), pgB = sub_page(k_begin + kTile), pgC = sub_page(k_begin + 2 * kTile);
+  issue_tile(a.k, Ks, k_begin, pgA);
+  issue_tile(a.v, Vs, k_begin, pgA);
+  if (ntiles > 1) issue_tile(a.k, Ks + kTileElems, k_begin + kTile, pgB);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  f32x4 scur[2][4];
+  if (wave_active) qk(Ks, scur);
+  __syncthreads();  // every wave has read K(0) before iteration 0 refills its buffer
+
+  // One pipeline step for tile `it` (buffer parity CUR = it & 1, a
+  // compile-time constant so LDS buffer bases fold into immediates).
+  auto step = [&](int it, auto cur_c) {
+    constexpr int cur = decltype(cur_c)::value;
+    const int t0 = k_begin + it * kTile;
+    // page ids: pgA <- tile t+1, pgB <- t+2, pgC <- t+3
+    pgA = pgB;
+    pgB = pgC;
+    pgC = sub_page(t0 + 3 * kTile);
+    // K(t+2) into the buffer K(t) left, V(t+1) into the one V(t-1) left.
+    if (it + 2 < ntiles) issue_tile(a.k, Ks + cur * kTileElems, t0 + 2 * kTile, pgB);
+    if (it + 1 < ntiles) issue_tile(a.v, Vs + (cur ^ 1) * kTileElems, t0 + kTile, pgA);
+    if (wave_active) {
+      f32x4 snext[2][4];
+      if (it + 1 < ntiles) qk(Ks + (cur ^ 1) * kTileElems, snext);
+      bf16x8 pb[2][2];
+      softmax(t0, scur, pb);
+      pv(Vs + cur * kTileElems, pb);
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) scur[nt][mt] = snext[nt][mt];
+    }
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+  };
+  for (int it = 0; it < ntiles; it += 2) {
+    step(it, std::integral_constant<int, 0>());
+    if (it + 1 < ntiles) step(it + 1, std::integral_constant<int, 1>());
   }
 
   // Epilogue: lane holds row l16 and head dims 16*dt + 4*lg + 0..3.
