@@ -8,28 +8,38 @@
 //
 // GPU design.  For one (sequence, KV head) all n * G query rows (G query
 // heads per KV head) share every K/V tile, so they are processed together:
-// a workgroup of 4 waves owns 128 rows (32 per wave, two 16-row MFMA tiles)
-// and streams one split of the key range in 64-key tiles.
-//   * K and V tiles are read from HBM with 16-byte coalesced loads,
-//     prefetched into registers one tile ahead, and staged in LDS (V is
-//     transposed on the way in).
-//   * S^T = K Q^T and O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 with
-//     fp32 accumulation.  In this orientation a query row lives in one lane
-//     column of both accumulators, so the online-softmax statistics and the
-//     rescale of O are lane-local, and the probabilities P feed the second
-//     MFMA straight from registers: the contraction index of P^T is
-//     permuted to match the S^T output layout and V^T is read with the same
-//     permutation.
-//   * Softmax uses exp2 with scale*log2(e) folded in; row max and sum need
-//     two cross-lane shuffles.  The ancestor mask is a bitset per tree node
-//     in LDS and is applied only on tiles that reach the tree positions or
-//     the end of the range.
+// a workgroup of 8 waves owns 256 rows (32 per wave) and streams one split
+// of the key range in 64-key tiles; one workgroup per CU.
+//   * Products run on v_mfma_f32_32x32x16_bf16 (the full-rate bf16 shape on
+//     gfx950) with fp32 accumulation: S^T = K Q^T (32 keys x 32 rows per
+//     MFMA) and O^T = V^T P^T (32 head dims x 32 rows).  In this orientation
+//     a query row lives in one lane column of both accumulators, so the
+//     online-softmax statistics and the rescale of O are lane-local (the
+//     two lane halves are merged with one permlane32 swap) and P feeds the
+//     second MFMA straight from registers: the contraction index of P^T is
+//     permuted to match the S^T output layout, and V^T is read with the same
+//     permutation by ds_read_b64_tr_b16 transposing reads.  The head-dim
+//     order inside each 32-row block of O^T is permuted too (lane halves of
+//     a transposing read take head dims D/2 apart), which the epilogue undoes.
+//   * K and V tiles are read from HBM with 16-byte buffer loads (one scalar
+//     descriptor per 8-key sub-block of a page, so tails read as zero),
+//     prefetched into registers one tile ahead and stored to double-buffered
+//     LDS.  LDS rows are padded (K by 16 bytes, V by 32) so that the operand
+//     reads of every MFMA are bank-conflict free and their addresses are one
+//     base register plus immediate offsets.
+//   * Softmax uses exp2 with scale*log2(e) folded in and a lazily raised
+//     reference maximum.  The ancestor mask is a bitset per tree node in LDS
+//     and is applied only on tiles that reach the tree positions or the end
+//     of the range.
 //   * Long contexts are split into fixed chunks of keys so the grid has
 //     enough independent work; each split writes unnormalised partial
 //     output plus (max, sum) and a small combine kernel merges them.  A
 //     sequence that fits in one chunk writes bf16 output directly.
-//   * Block ids are remapped so that the row blocks and splits of one
-//     (sequence, KV head) run on the same XCD and share its L2.
+//   * Work is scheduled by a small plan kernel that lists the (sequence, KV
+//     head, split, row block) items that have work, longest first; one
+//     persistent workgroup per CU takes items from an atomic counter, so no
+//     CU idles on empty grid slots and long items do not form a tail.
+#include <algorithm>
 #include <cmath>
 #include <type_traits>
 
@@ -41,14 +51,18 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * SRT_WAVE;
-constexpr int kRowsPerBlock = kWaves * 32;
-constexpr int kTile = 64;      // keys per tile
-constexpr int kMaxN = 256;     // tree rows
-constexpr int kChunk = 4096;   // keys per split
-constexpr int kXcds = 8;
+constexpr int kRowsPerWave = 32;
+constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
+constexpr int kTile = 64;                  // keys per tile
+constexpr int kSubRows = kTile / kWaves;   // keys of each tile one wave stages
+constexpr int kMaxN = 256;                 // tree rows
+constexpr int kChunk = 4096;               // keys per split
 
 struct AttnArgs {
   const uint16_t* q;
@@ -61,16 +75,33 @@ struct AttnArgs {
   uint16_t* out;
   float* part_o;
   float* part_ml;
+  int32_t* plan;  // work list built by the plan kernel
   int32_t B, N, Hq, Hkv, G, page, page_shift, max_pages;
   int64_t num_pages;
   float scale_log2;
   int32_t S, RB, total;
 };
 
+// Work list: plan[0] = number of items, plan[1] = next item to hand out,
+// then item i at plan[kPlanHeader + 2 i] = sequence, [.. + 1] = KV head |
+// split << 8 | row block << 20.  Items are ordered by decreasing cost
+// (tiles, then active waves) so that the longest ones start first.
+constexpr int kPlanHeader = 64;
+constexpr int kPlanKeys = (kChunk / kTile) * kWaves;  // (tiles, waves) classes
+
+__device__ inline int plan_key(int tiles, int waves) {  // 0 = most expensive
+  return kPlanKeys - 1 - ((tiles - 1) * kWaves + (waves - 1));
+}
+
 template <int D>
 struct Shape {
-  static constexpr int KD = D / 32;      // MFMA steps over the head dimension
-  static constexpr int DT = D / 16;      // 16-wide blocks of the head dimension
+  static constexpr int KS = D / 16;            // k-steps of S^T = K Q^T
+  static constexpr int DB = D / 32;            // 32-dim blocks of O^T
+  static constexpr int CPR = D / 8;            // 16-byte chunks per K/V row
+  static constexpr int KSTRIDE = 2 * D + 16;   // LDS bytes per K row
+  static constexpr int VSTRIDE = 2 * D + 32;   // LDS bytes per V row
+  static constexpr int KTILE = kTile * KSTRIDE;
+  static constexpr int VTILE = kTile * VSTRIDE;
 };
 
 __device__ inline uint16_t to_bf16_bits(float x) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x)); }
@@ -88,43 +119,69 @@ __device__ inline SeqInfo seq_info(const AttnArgs& a, int b) {
   return s;
 }
 
-// Loads kLoads x 1 KB from `base` (nbytes valid, the rest reads as zero)
-// straight into LDS: load j writes lds + j*stride_elems, lane l's 16 bytes
-// (from byte offset voff[j]) at offset 16*l.
-template <int kLoads>
-__device__ inline void buffer_to_lds(const uint16_t* base, int nbytes, uint16_t* lds, int stride_elems,
-                                     const int (&voff)[kLoads]) {
-  const __amdgpu_buffer_rsrc_t rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, nbytes, 0x00020000);
+// Buffer descriptor over `nbytes` bytes at `base` (loads past nbytes read 0).
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base, int nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, nbytes, 0x00020000);
+}
+
+// kLoads 16-byte loads through one descriptor: lane byte offset voff plus
+// j * step for load j.
+template <int kLoads, int kStep>
+__device__ inline void buffer_load16(const uint16_t* base, int nbytes, int voff, uint4 (&r)[kLoads]) {
+  const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(base, nbytes);
 #pragma unroll
-  for (int j = 0; j < kLoads; ++j)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(lds + j * stride_elems),
-                                             16, voff[j], 0, 0, 0);
+  for (int j = 0; j < kLoads; ++j) {
+    typedef int i32x4 __attribute__((ext_vector_type(4)));
+    const i32x4 x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff + j * kStep, 0, 0);
+    r[j] = __builtin_bit_cast(uint4, x);
+  }
+}
+
+// The two 32-lane halves of x exchanged by v_permlane32_swap: returns
+// {x, x of lane ^ 32} in some order.  (Each result element is copied to a
+// scalar before the bit cast: a bit cast of a vector element reads
+// element 0 with this compiler.)
+__device__ inline void swap_halves(float x, float& u, float& v) {
+  const unsigned a = __builtin_bit_cast(unsigned, x);
+  const auto s = __builtin_amdgcn_permlane32_swap(a, a, false, false);
+  const unsigned s0 = s[0], s1 = s[1];
+  u = __builtin_bit_cast(float, s0);
+  v = __builtin_bit_cast(float, s1);
+}
+
+// Maximum / sum over the two 32-lane halves, result in every lane.
+__device__ inline float max_halves(float x) {
+  float u, v;
+  swap_halves(x, u, v);
+  return __builtin_elementwise_maximum(u, v);
+}
+
+__device__ inline float sum_halves(float x) {
+  float u, v;
+  swap_halves(x, u, v);
+  return u + v;
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   using Sh = Shape<D>;
-  constexpr int CPR = D / 8;                 // 16-byte chunks per K/V row
-  constexpr int kTileElems = kTile * D;      // unpadded, chunk-swizzled rows
-  // K is consumed one tile before V (pipelining below), so each has its own
-  // pair of LDS buffers.
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * kTileElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2 * kTileElems];
+  constexpr int CPR = Sh::CPR;
+  __shared__ __attribute__((aligned(16))) uint8_t Ks[2 * Sh::KTILE];
+  __shared__ __attribute__((aligned(16))) uint8_t Vs[2 * Sh::VTILE];
   __shared__ uint64_t anc[kMaxN][4];
   __shared__ int32_t spar[kMaxN];
 
-  const int nb = gridDim.x;
-  const int item = (blockIdx.x % kXcds) * (nb / kXcds) + blockIdx.x / kXcds;
-  if (item >= a.total) return;
-  int rest = item;
-  const int rb = rest % a.RB;
-  rest /= a.RB;
-  const int s = rest % a.S;
-  rest /= a.S;
-  const int g = rest % a.Hkv;
-  const int b = rest / a.Hkv;
+  __shared__ int32_t s_item;
+  const int tid = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(tid / SRT_WAVE);  // wave-uniform, in an SGPR
+  const int lane = tid % SRT_WAVE;
+  const int l32 = lane % 32;  // query row of this lane inside the wave's 32
+  const int h = lane / 32;    // lane half
+  const int n_items = a.plan[0];
 
+  // Persistent workgroups: each takes the next item of the work list until
+  // the list is exhausted.
+  auto run_item = [&](const int b, const int g, const int s, const int rb) {
   const SeqInfo si = seq_info(a, b);
   const int rows = si.n * a.G;
   if (rb * kRowsPerBlock >= rows) return;
@@ -132,13 +189,8 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
   if (k_begin >= si.total) return;
   const int k_end = min(k_begin + kChunk, si.total);
   const int nsplit = (si.total + kChunk - 1) / kChunk;
-
-  const int tid = threadIdx.x;
-  const int w = __builtin_amdgcn_readfirstlane(tid / SRT_WAVE);  // wave-uniform, in an SGPR
-  const int lane = tid % SRT_WAVE;
-  const int l16 = lane % 16;
-  const int lg = lane / 16;
-  const int row0 = rb * kRowsPerBlock + w * 32;
+  const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
+  const int row0 = rb * kRowsPerBlock + w * kRowsPerWave;
   const bool wave_active = row0 < rows;  // wave-uniform
 
   // Ancestor-or-self bitsets, needed only when this split reaches the tree.
@@ -159,237 +211,241 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
     }
   }
 
-  // Query fragments: B operand of S^T = K Q^T (lane: row l16, head dims 8*lg..+7).
-  bf16x8 qf[2][Sh::KD];
-  int node_of[2];
-  bool row_ok[2];
+  // Query fragment: B operand of S^T = K Q^T; lane holds row l32 and head
+  // dims 16 ks + 8 h .. +7 for k-step ks.
+  const int row = row0 + l32;
+  const bool row_ok = row < rows;
+  const int node = row_ok ? row / a.G : 0;
+  bf16x8 qf[Sh::KS];
+  {
+    const int hq = g * a.G + (row_ok ? row % a.G : 0);
+    const bf16x8* qp =
+        reinterpret_cast<const bf16x8*>(a.q + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + hq) * D + 8 * h);
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    const int r = row0 + nt * 16 + l16;
-    row_ok[nt] = r < rows;
-    const int node = row_ok[nt] ? r / a.G : 0;
-    const int h = g * a.G + (row_ok[nt] ? r % a.G : 0);
-    node_of[nt] = node;
-    const bf16x8* qp = reinterpret_cast<const bf16x8*>(
-        a.q + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + h) * D + 8 * lg);
-#pragma unroll
-    for (int kd = 0; kd < Sh::KD; ++kd) qf[nt][kd] = row_ok[nt] ? qp[4 * kd] : bf16x8{};
+    for (int ks = 0; ks < Sh::KS; ++ks) qf[ks] = row_ok ? qp[2 * ks] : bf16x8{};
   }
 
-  f32x4 o[2][Sh::DT];
+  f32x16 o[Sh::DB];
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt)
+  for (int db = 0; db < Sh::DB; ++db)
 #pragma unroll
-    for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // Reference maximum (log2 units) and lane-partial sums per row tile.  The
-  // reference is raised only when a row's maximum exceeds it by more than
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
+  // Reference maximum (log2 units) and lane-partial sum of the row.  The
+  // reference is raised only when the row maximum exceeds it by more than
   // kLazy, so most tiles need no rescale of O.
   constexpr float kLazy = 8.f;
-  float m[2] = {-INFINITY, -INFINITY};
-  float l[2] = {0.f, 0.f};
+  float m = -INFINITY;
+  float l = 0.f;
   const float c = a.scale_log2;
 
   // ---- staging ----------------------------------------------------------
-  // K and V tiles go straight from HBM to LDS (buffer loads with the LDS
-  // destination; no staging registers).  Wave w moves the w-th 16-key
-  // sub-block of a tile, which lies inside one page (pages are powers of two
-  // >= 16): one buffer descriptor covers exactly its valid keys, so keys past
-  // the split end or on an invalid page read as zero.  Row r's 16-byte chunk
-  // c is stored at chunk position c ^ (r % CPR) (conflict-free operand reads);
-  // a load instruction writes 1 KB contiguous, lane l at offset 16*l, so lane
-  // l fetches the chunk that belongs at its position.
+  // Wave w moves keys 8w .. 8w+7 of every K and V tile; they lie inside one
+  // page (pages are powers of two >= 16), so one scalar buffer descriptor
+  // covers exactly the valid keys and keys past the split end or on an
+  // invalid page read as zero.  Loads go to registers one tile ahead and are
+  // stored to LDS after the tile's compute.
   const int pshift = a.page_shift;
   const int pmask = (1 << pshift) - 1;
   const int64_t bt_row = static_cast<int64_t>(b) * a.max_pages;
-  const int32_t __attribute__((address_space(4)))* btc =
-      (const int32_t __attribute__((address_space(4)))*)(a.bt) + bt_row;
   const int64_t head_stride = static_cast<int64_t>(a.page) * D;  // elements per (page, head)
-  constexpr int kRowsPerLoad = 1024 / (2 * D);                    // 4 (d=128) or 8 (d=64)
-  constexpr int kLoadsPerWave = 16 / kRowsPerLoad;                // per tile, per tensor
-  // Per-lane byte offset inside the sub-block and LDS placement of each load.
-  int lane_voff[kLoadsPerWave];
-#pragma unroll
-  for (int j = 0; j < kLoadsPerWave; ++j) {
-    const int r = kRowsPerLoad * j + lane / CPR;     // row within the sub-block (0..15)
-    const int pos = lane % CPR;                      // chunk position written by this lane
-    const int row = 16 * w + r;                      // row within the tile
-    const int chunk = pos ^ (row & (CPR - 1));
-    lane_voff[j] = (r * D + chunk * 8) * 2;
-  }
+  constexpr int kRowsPerLoad = SRT_WAVE / CPR;                    // 4 (d=128) or 8 (d=64)
+  constexpr int kLoadsPerWave = kSubRows / kRowsPerLoad;          // per tile, per tensor
+  static_assert(kLoadsPerWave >= 1 && kSubRows % kRowsPerLoad == 0, "staging shape");
+  const int st_row = kSubRows * w + lane / CPR;  // tile row of this lane's first chunk
+  const int gl_off = ((lane / CPR) * D + (lane % CPR) * 8) * 2;
+  const int k_st = st_row * Sh::KSTRIDE + (lane % CPR) * 16;
+  const int v_st = st_row * Sh::VSTRIDE + (lane % CPR) * 16;
 
-  // Page id of this wave's sub-block of the tile at t0 (-1 if none).
-  auto sub_page = [&](int t0) {
-    const int p0 = t0 + 16 * w;
-    return p0 < k_end ? btc[p0 >> pshift] : -1;
-  };
-  auto issue_tile = [&](const uint16_t* src, uint16_t* dst, int t0, int pg) {
-    const int p0 = t0 + 16 * w;
+  // Page ids of this wave's sub-block of every tile of the split, one tile
+  // per lane (a split has exactly 64 tiles), fetched once; the loop reads
+  // them with v_readlane and touches no block-table memory.
+  static_assert(kChunk / kTile == SRT_WAVE, "one lane per tile of a split");
+  int pg_lane;
+  {
+    const int p0 = k_begin + kTile * lane + kSubRows * w;
+    pg_lane = p0 < k_end ? a.bt[bt_row + (p0 >> pshift)] : -1;
+  }
+  auto page_of = [&](int it) { return it < ntiles ? __builtin_amdgcn_readlane(pg_lane, it) : -1; };
+  uint4 kreg[kLoadsPerWave], vreg[kLoadsPerWave];
+  auto load_sub = [&](const uint16_t* base, int t0, int pg, uint4 (&r)[kLoadsPerWave]) {
+    const int p0 = t0 + kSubRows * w;
     const bool ok = pg >= 0 && pg < a.num_pages && p0 < k_end;
-    const int nkeys = ok ? min(16, k_end - p0) : 0;
-    const uint16_t* base = ok ? src + (static_cast<int64_t>(pg) * a.Hkv + g) * head_stride + (p0 & pmask) * D : src;
-    buffer_to_lds<kLoadsPerWave>(base, nkeys * D * 2, dst + 16 * w * D, kRowsPerLoad * D, lane_voff);
+    const int nbytes = ok ? min(kSubRows, k_end - p0) * D * 2 : 0;
+    const int64_t off = ok ? (static_cast<int64_t>(pg) * a.Hkv + g) * head_stride + (p0 & pmask) * D : 0;
+    buffer_load16<kLoadsPerWave, kRowsPerLoad * D * 2>(base + off, nbytes, gl_off, r);
+  };
+  auto store_k = [&](uint8_t* Kb) {
+#pragma unroll
+    for (int j = 0; j < kLoadsPerWave; ++j) *reinterpret_cast<uint4*>(Kb + k_st + j * kRowsPerLoad * Sh::KSTRIDE) = kreg[j];
+  };
+  auto store_v = [&](uint8_t* Vb) {
+#pragma unroll
+    for (int j = 0; j < kLoadsPerWave; ++j) *reinterpret_cast<uint4*>(Vb + v_st + j * kRowsPerLoad * Sh::VSTRIDE) = vreg[j];
   };
 
   // ---- MFMA phases -------------------------------------------------------
-  // Lane offsets (elements) of the swizzled operand reads.  For K the XOR
-  // term depends only on the lane's row within a 16-row group, so row groups
-  // (mt) add a constant; for V it depends on the row within 16 as well, so
-  // ks and the +16-row half add constants.  Only the head-dim index varies
-  // non-linearly and gets its own register.
-  int koff[Sh::KD];
-#pragma unroll
-  for (int kd = 0; kd < Sh::KD; ++kd) koff[kd] = (l16 * CPR + ((4 * kd + lg) ^ (l16 & (CPR - 1)))) * 8;
-  int voff[Sh::DT];
-  {
-    const int r0 = 4 * lg + l16 / 4;  // row within the 32-row group, < 16
-#pragma unroll
-    for (int dt = 0; dt < Sh::DT; ++dt)
-      voff[dt] = (r0 * CPR + ((2 * dt + ((l16 & 3) >> 1)) ^ (r0 & (CPR - 1)))) * 8 + (l16 & 1) * 4;
-  }
+  // K operand (A of S^T): lane reads key l32 (+32 kb), head dims
+  // 16 ks + 8 h .. +7.
+  const int k_rd = l32 * Sh::KSTRIDE + 16 * h;
+  // V^T operand (A of O^T) by transposing reads: in each 16-lane group G,
+  // lane x addresses key 16 ks + 4 h + x/4 (+8 for the second half of the
+  // contraction) and head dims (D/2)(G%2) + 16 db + 4 (x%4) .. +3.
+  const int xg = lane % 16;
+  const int k_vd = (4 * h + xg / 4) * Sh::VSTRIDE + ((CPR / 2) * ((lane / 16) & 1) + (xg % 4) / 2) * 16 + 8 * (xg & 1);
 
-  // S^T[key][row] of one tile: 4 key groups x 2 row tiles.
-  auto qk = [&](const uint16_t* Kb, f32x4 (&sacc)[2][4]) {
+  // S^T[key][row] of one tile: two 32-key blocks.
+  auto qk = [&](const uint8_t* Kb, f32x16 (&sacc)[2]) {
+    // All fragment reads are issued before the first MFMA so that one LDS
+    // latency, not one per k-step, is exposed.
+    bf16x8 kf[Sh::KS][2];
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
+    for (int ks = 0; ks < Sh::KS; ++ks)
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) sacc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kb = 0; kb < 2; ++kb)
+        kf[ks][kb] = *reinterpret_cast<const bf16x8*>(Kb + k_rd + kb * 32 * Sh::KSTRIDE + ks * 32);
 #pragma unroll
-    for (int kd = 0; kd < Sh::KD; ++kd) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Kb + 16 * mt * D + koff[kd]);
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          sacc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[nt][kd], sacc[nt][mt], 0, 0, 0);
-      }
-    }
+    for (int ks = 0; ks < Sh::KS; ++ks)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][kb], qf[ks], sacc[kb], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * Sh::KS, 0);  // DS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * Sh::KS, 0);  // then MFMAs
   };
 
-  // Mask, online softmax with lazy rescale; returns P in bf16.
-  auto softmax = [&](int t0, f32x4 (&sacc)[2][4], bf16x8 (&pb)[2][2]) {
+  // Mask, online softmax with lazy rescale; returns P in bf16.  Lane holds
+  // keys 32 kb + 8 (r/4) + 4 h + r%4 of its row in sacc[kb][r].
+  auto softmax = [&](int t0, f32x16 (&sacc)[2], bf16x8 (&pb)[4]) {
     const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
+    if (need_mask) {
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      if (need_mask) {
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x16 t = sacc[kb];
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-          f32x4 t = sacc[nt][mt];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int pos = t0 + 16 * mt + 4 * lg + r;
-            bool vis = pos < k_end;
-            if (vis && pos >= si.L) {
-              const int j = pos - si.L;
-              vis = (anc[node_of[nt]][j >> 6] >> (j & 63)) & 1ull;
-            }
-            t[r] = vis ? t[r] : -INFINITY;
+        for (int r = 0; r < 16; ++r) {
+          const int pos = t0 + 32 * kb + 8 * (r / 4) + 4 * h + r % 4;
+          bool vis = pos < k_end;
+          if (vis && pos >= si.L) {
+            const int j = pos - si.L;
+            vis = (anc[node][j >> 6] >> (j & 63)) & 1ull;
           }
-          sacc[nt][mt] = t;
+          t[r] = vis ? t[r] : -INFINITY;
         }
-      }
-      float mloc = fmaxf(fmaxf(sacc[nt][0][0], sacc[nt][0][1]), fmaxf(sacc[nt][0][2], sacc[nt][0][3]));
-#pragma unroll
-      for (int mt = 1; mt < 4; ++mt)
-        mloc = fmaxf(mloc, fmaxf(fmaxf(sacc[nt][mt][0], sacc[nt][mt][1]), fmaxf(sacc[nt][mt][2], sacc[nt][mt][3])));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, SRT_WAVE));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, SRT_WAVE));
-      const float ms = mloc * c;  // row max in log2 units (c > 0)
-      const bool raise = ms > m[nt] + kLazy;
-      if (__ballot(raise)) {
-        const float mnew = raise ? ms : m[nt];
-        const float alpha = m[nt] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
-        l[nt] *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < Sh::DT; ++dt) o[nt][dt] *= alpha;
-        m[nt] = mnew;
-      }
-      const float mref = m[nt] == -INFINITY ? 0.f : m[nt];
-      float psum = 0.f;
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[nt][mt][r], c, -mref));
-          sacc[nt][mt][r] = p;
-          psum += p;
-        }
-      }
-      l[nt] += psum;
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          pb[nt][ks][r] = static_cast<__bf16>(sacc[nt][2 * ks][r]);
-          pb[nt][ks][4 + r] = static_cast<__bf16>(sacc[nt][2 * ks + 1][r]);
-        }
+        sacc[kb] = t;
       }
     }
-  };
-
-  // O^T[d][row] += V^T P^T.  Contraction index (8*lg + e) <-> key
-  // 32*ks + 16*(e/4) + 4*lg + e%4, matching the S^T layout; the V^T operand
-  // comes from transposing LDS reads: lane (lg, l16) addresses row
-  // 32*ks + 4*lg + l16/4 (+16), head dims 16*dt + 4*(l16%4) .. +3.
-  auto pv = [&](const uint16_t* Vb, const bf16x8 (&pb)[2][2]) {
-    typedef short i16x4 __attribute__((ext_vector_type(4)));
-    typedef short i16x8 __attribute__((ext_vector_type(8)));
+    // (maximum, not fmaxf: no NaN-quieting of every operand; scores are
+    // finite or -inf)
+    float mloc = -INFINITY;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int dt = 0; dt < Sh::DT; ++dt) {
-        const uint16_t* p0 = Vb + 32 * ks * D + voff[dt];
-        const uint16_t* p1 = p0 + 16 * D;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p1));
-        const i16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        const bf16x8 va = __builtin_bit_cast(bf16x8, both);
+      for (int r = 0; r < 16; r += 2)
+        mloc = __builtin_elementwise_maximum(mloc, __builtin_elementwise_maximum(sacc[kb][r], sacc[kb][r + 1]));
+    mloc = max_halves(mloc);
+    const float ms = mloc * c;  // row max in log2 units (c > 0)
+    const bool raise = ms > m + kLazy;
+    if (__ballot(raise)) {
+      const float mnew = raise ? ms : m;
+      const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mnew);
+      l *= alpha;
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[nt][ks], o[nt][dt], 0, 0, 0);
-      }
+      for (int db = 0; db < Sh::DB; ++db) o[db] *= alpha;
+      m = mnew;
     }
+    const float mref = m == -INFINITY ? 0.f : m;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][r], c, -mref));
+    // Contraction index 8 h + e of k-step ks <-> key 16 ks + 8 (e/4) + 4 h + e%4.
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pb[ks][e] = static_cast<__bf16>(sacc[ks / 2][8 * (ks % 2) + e]);
+    // Row sum of the probabilities as rounded for the second product (two
+    // bf16 pairs per dot2, two accumulators).
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 one2 = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+    float ps[2] = {0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const bf16x2 pr = {pb[ks][e], pb[ks][e + 1]};
+        ps[ks & 1] = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, ps[ks & 1], false);
+      }
+    l += ps[0] + ps[1];
   };
 
-  // ---- software pipeline -------------------------------------------------
-  // Iteration t: global loads of K(t+2) and V(t+1) are issued; S(t+1) = K Q^T
-  // of the next tile runs on the MFMA pipe while softmax(t) runs on the VALU;
-  // then O += V(t)^T P(t); finally K(t+2) and V(t+1) go to the buffers that
-  // K(t) and V(t-1) have left.  One barrier per tile.
-  const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
-  int pgA = sub_page(k_begin), pgB = sub_page(k_begin + kTile), pgC = sub_page(k_begin + 2 * kTile);
-  issue_tile(a.k, Ks, k_begin, pgA);
-  issue_tile(a.v, Vs, k_begin, pgA);
-  if (ntiles > 1) issue_tile(a.k, Ks + kTileElems, k_begin + kTile, pgB);
-  __builtin_amdgcn_s_waitcnt(0);
+  // O^T[d][row] += V^T P^T.
+  // V^T fragments of k-steps ks0, ks0+1 (two transposing reads per MFMA).
+  typedef short i16x4v __attribute__((ext_vector_type(4)));
+  auto v_read = [&](const uint8_t* Vb, int ks0, i16x4v (&vf)[2][Sh::DB][2]) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+      for (int db = 0; db < Sh::DB; ++db)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+          vf[k2][db][hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) i16x4v*)(Vb + k_vd + (ks0 + k2) * 16 * Sh::VSTRIDE +
+                                                          hh * 8 * Sh::VSTRIDE + db * 32));
+  };
+  auto pv = [&](const i16x4v (&vf)[2][Sh::DB][2], int ks0, const bf16x8 (&pb)[4]) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+      for (int db = 0; db < Sh::DB; ++db) {
+        const bf16x8 va =
+            __builtin_bit_cast(bf16x8, __builtin_shufflevector(vf[k2][db][0], vf[k2][db][1], 0, 1, 2, 3, 4, 5, 6, 7));
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks0 + k2], o[db], 0, 0, 0);
+      }
+  };
+
+  // ---- tile loop ---------------------------------------------------------
+  // Iteration t: global loads of tile t+1 are issued to registers; the K
+  // fragments of tile t are read from LDS and S = K Q^T runs; the V^T
+  // fragments are read while softmax runs on the VALU; O += V^T P^T; then
+  // tile t+1 is stored into the buffers tile t-1 left.  One barrier per tile.
+  {
+    const int pg0 = page_of(0);
+    load_sub(a.k, k_begin, pg0, kreg);
+    load_sub(a.v, k_begin, pg0, vreg);
+    store_k(Ks);
+    store_v(Vs);
+  }
   __syncthreads();
-  f32x4 scur[2][4];
-  if (wave_active) qk(Ks, scur);
-  __syncthreads();  // every wave has read K(0) before iteration 0 refills its buffer
 
-  // One pipeline step for tile `it` (buffer parity CUR = it & 1, a
-  // compile-time constant so LDS buffer bases fold into immediates).
   auto step = [&](int it, auto cur_c) {
     constexpr int cur = decltype(cur_c)::value;
     const int t0 = k_begin + it * kTile;
-    // page ids: pgA <- tile t+1, pgB <- t+2, pgC <- t+3
-    pgA = pgB;
-    pgB = pgC;
-    pgC = sub_page(t0 + 3 * kTile);
-    // K(t+2) into the buffer K(t) left, V(t+1) into the one V(t-1) left.
-    if (it + 2 < ntiles) issue_tile(a.k, Ks + cur * kTileElems, t0 + 2 * kTile, pgB);
-    if (it + 1 < ntiles) issue_tile(a.v, Vs + (cur ^ 1) * kTileElems, t0 + kTile, pgA);
-    if (wave_active) {
-      f32x4 snext[2][4];
-      if (it + 1 < ntiles) qk(Ks + (cur ^ 1) * kTileElems, snext);
-      bf16x8 pb[2][2];
-      softmax(t0, scur, pb);
-      pv(Vs + cur * kTileElems, pb);
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) scur[nt][mt] = snext[nt][mt];
+    const bool next = it + 1 < ntiles;
+    if (next) {
+      const int pg = page_of(it + 1);
+      load_sub(a.k, t0 + kTile, pg, kreg);
+      load_sub(a.v, t0 + kTile, pg, vreg);
     }
-    __builtin_amdgcn_s_waitcnt(0);
+    if (wave_active) {
+      f32x16 sacc[2];
+      qk(Ks + cur * Sh::KTILE, sacc);
+      // First half of the V^T fragments is read while softmax runs, the
+      // second half while the first half's MFMAs run.
+      i16x4v vf0[2][Sh::DB][2], vf1[2][Sh::DB][2];
+      v_read(Vs + cur * Sh::VTILE, 0, vf0);
+      bf16x8 pb[4];
+      softmax(t0, sacc, pb);
+      v_read(Vs + cur * Sh::VTILE, 2, vf1);
+      pv(vf0, 0, pb);
+      pv(vf1, 2, pb);
+    }
+    if (next) {
+      store_k(Ks + (cur ^ 1) * Sh::KTILE);
+      store_v(Vs + (cur ^ 1) * Sh::VTILE);
+    }
     __syncthreads();
   };
   for (int it = 0; it < ntiles; it += 2) {
@@ -397,36 +453,103 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_kernel(AttnArgs a) {
     if (it + 1 < ntiles) step(it + 1, std::integral_constant<int, 1>());
   }
 
-  // Epilogue: lane holds row l16 and head dims 16*dt + 4*lg + 0..3.
+  // Epilogue: lane holds row l32 and, for block db and quad q = r/4, head
+  // dims (D/2)(q/2) + 16 db + 8 (q%2) + 4 h + 0..3.
+  const float lt = sum_halves(l);
+  if (!row_ok) return;
   const int RBR = a.RB * kRowsPerBlock;
+  if (nsplit == 1) {
+    const int hq = g * a.G + row % a.G;
+    uint16_t* op = a.out + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + hq) * D + 4 * h;
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    float lt = l[nt];
-    lt += __shfl_xor(lt, 16, SRT_WAVE);
-    lt += __shfl_xor(lt, 32, SRT_WAVE);
-    if (!row_ok[nt]) continue;
-    const int r = row0 + nt * 16 + l16;
-    if (nsplit == 1) {
-      const int h = g * a.G + r % a.G;
-      uint16_t* op = a.out + ((static_cast<int64_t>(b) * a.N + r / a.G) * a.Hq + h) * D + 4 * lg;
-      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    for (int db = 0; db < Sh::DB; ++db) {
 #pragma unroll
-      for (int dt = 0; dt < Sh::DT; ++dt) {
-        const uint32_t x0 = to_bf16_bits(o[nt][dt][0] * inv) | (uint32_t(to_bf16_bits(o[nt][dt][1] * inv)) << 16);
-        const uint32_t x1 = to_bf16_bits(o[nt][dt][2] * inv) | (uint32_t(to_bf16_bits(o[nt][dt][3] * inv)) << 16);
-        *reinterpret_cast<uint2*>(op + 16 * dt) = make_uint2(x0, x1);
-      }
-    } else {
-      const int64_t prow = ((static_cast<int64_t>(b) * a.Hkv + g) * a.S + s) * RBR + r;
-      float* po = a.part_o + prow * D + 4 * lg;
-#pragma unroll
-      for (int dt = 0; dt < Sh::DT; ++dt) *reinterpret_cast<f32x4*>(po + 16 * dt) = o[nt][dt];
-      if (lg == 0) {
-        a.part_ml[2 * prow] = m[nt];
-        a.part_ml[2 * prow + 1] = lt;
+      for (int q = 0; q < 4; ++q) {
+        const int d0 = (D / 2) * (q / 2) + 16 * db + 8 * (q % 2);
+        const uint32_t x0 =
+            to_bf16_bits(o[db][4 * q] * inv) | (uint32_t(to_bf16_bits(o[db][4 * q + 1] * inv)) << 16);
+        const uint32_t x1 =
+            to_bf16_bits(o[db][4 * q + 2] * inv) | (uint32_t(to_bf16_bits(o[db][4 * q + 3] * inv)) << 16);
+        *reinterpret_cast<uint2*>(op + d0) = make_uint2(x0, x1);
       }
     }
+  } else {
+    const int64_t prow = ((static_cast<int64_t>(b) * a.Hkv + g) * a.S + s) * RBR + row;
+    float* po = a.part_o + prow * D + 4 * h;
+#pragma unroll
+    for (int db = 0; db < Sh::DB; ++db) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int d0 = (D / 2) * (q / 2) + 16 * db + 8 * (q % 2);
+        *reinterpret_cast<f32x4*>(po + d0) = f32x4{o[db][4 * q], o[db][4 * q + 1], o[db][4 * q + 2], o[db][4 * q + 3]};
+      }
+    }
+    if (h == 0) {
+      a.part_ml[2 * prow] = m;
+      a.part_ml[2 * prow + 1] = lt;
+    }
   }
+  };
+
+  for (;;) {
+    if (tid == 0) s_item = atomicAdd(a.plan + 1, 1);
+    __syncthreads();
+    const int idx = s_item;
+    if (idx >= n_items) break;
+    const int b = a.plan[kPlanHeader + 2 * idx];
+    const int packed = a.plan[kPlanHeader + 2 * idx + 1];
+    run_item(b, packed & 0xff, (packed >> 8) & 0xfff, packed >> 20);
+    __syncthreads();  // LDS and s_item are reused by the next item
+  }
+}
+
+// Builds the work list: one item per (sequence, KV head, split, row block)
+// that has work, counting-sorted by decreasing (tiles, active waves).  One
+// workgroup; also resets the hand-out counter.
+__global__ __launch_bounds__(1024) void tree_attn_plan_kernel(AttnArgs a) {
+  __shared__ int32_t cnt[kPlanKeys], off[kPlanKeys], fill[kPlanKeys];
+  const int tid = threadIdx.x;
+  for (int k = tid; k < kPlanKeys; k += 1024) {
+    cnt[k] = 0;
+    fill[k] = 0;
+  }
+  __syncthreads();
+  // Visits the item classes of sequence b: f(key, first split, splits).
+  auto classes = [&](int b, auto&& f) {
+    const SeqInfo si = seq_info(a, b);
+    const int rows = si.n * a.G;
+    const int rbs = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
+    const int full = si.total / kChunk;
+    const int tail = si.total - full * kChunk;
+    for (int rb = 0; rb < rbs; ++rb) {
+      const int waves = min(kWaves, (rows - rb * kRowsPerBlock + kRowsPerWave - 1) / kRowsPerWave);
+      if (full > 0) f(plan_key(kChunk / kTile, waves), 0, full, rb);
+      if (tail > 0) f(plan_key((tail + kTile - 1) / kTile, waves), full, 1, rb);
+    }
+  };
+  for (int b = tid; b < a.B; b += 1024)
+    classes(b, [&](int key, int, int ns, int) { atomicAdd(&cnt[key], ns * a.Hkv); });
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int k = 0; k < kPlanKeys; ++k) {
+      off[k] = run;
+      run += cnt[k];
+    }
+    a.plan[0] = run;
+    a.plan[1] = 0;
+  }
+  __syncthreads();
+  for (int b = tid; b < a.B; b += 1024)
+    classes(b, [&](int key, int s0, int ns, int rb) {
+      int pos = off[key] + atomicAdd(&fill[key], ns * a.Hkv);
+      for (int s = s0; s < s0 + ns; ++s)
+        for (int g = 0; g < a.Hkv; ++g, ++pos) {
+          a.plan[kPlanHeader + 2 * pos] = b;
+          a.plan[kPlanHeader + 2 * pos + 1] = g | (s << 8) | (rb << 20);
+        }
+    });
 }
 
 // Merges the split partials of sequences that needed more than one split.
@@ -474,16 +597,31 @@ int splits_for(int32_t page, int32_t max_pages) {
   return static_cast<int>((cap + kChunk - 1) / kChunk);
 }
 
+// Bytes of the work list for at most B * Hkv * S * RB items, rounded to 256.
+size_t plan_bytes(int64_t items) { return ((kPlanHeader + 2 * items) * sizeof(int32_t) + 255) / 256 * 256; }
+
+int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+  if (dev < 64 && cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
+  if (dev < 64) cached[dev] = n;
+  return n;
+}
+
 }  // namespace
 
 extern "C" size_t srt_tree_attn_scratch_bytes(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d, int32_t page,
                                               int32_t max_pages) {
   if (B < 0 || N < 1 || N > kMaxN || Hq < 1 || Hkv < 1 || Hq % Hkv || page < 1 || max_pages < 1) return 0;
   const int S = splits_for(page, max_pages);
-  if (S <= 1) return 0;
   const int G = Hq / Hkv;
-  const int64_t RBR = static_cast<int64_t>((N * G + kRowsPerBlock - 1) / kRowsPerBlock) * kRowsPerBlock;
-  return static_cast<size_t>(B) * Hkv * S * RBR * (d + 2) * sizeof(float);
+  const int64_t RB = (N * G + kRowsPerBlock - 1) / kRowsPerBlock;
+  const size_t plan = plan_bytes(static_cast<int64_t>(B) * Hkv * S * RB);
+  if (S <= 1) return plan;
+  return plan + static_cast<size_t>(B) * Hkv * S * RB * kRowsPerBlock * (d + 2) * sizeof(float);
 }
 
 extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d, int32_t page,
@@ -496,11 +634,15 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
   if (!(scale == scale)) return SRT_ERR_INVALID;
   if (d != 64 && d != 128) return SRT_ERR_UNSUPPORTED;
   if (page < 16 || (page & (page - 1))) return SRT_ERR_UNSUPPORTED;
+  // work-list packing: KV head < 256, split < 4096, row block < 2048
+  if (Hkv > 255 || splits_for(page, max_pages) > 4095 || (N * (Hq / Hkv)) / kRowsPerBlock > 2046)
+    return SRT_ERR_UNSUPPORTED;
   if (B == 0) return SRT_OK;
   if (!q || !k_cache || !v_cache || !block_table || !ctx_len || !tree_parent || !n_nodes || !out)
     return SRT_ERR_INVALID;
   const size_t need = srt_tree_attn_scratch_bytes(B, N, Hq, Hkv, d, page, max_pages);
-  if (need > 0 && (!scratch || scratch_bytes < need)) return SRT_ERR_CAPACITY;
+  if (!scratch || scratch_bytes < need) return SRT_ERR_CAPACITY;
+  if (reinterpret_cast<uintptr_t>(scratch) % 256) return SRT_ERR_INVALID;
 
   AttnArgs a;
   a.q = q;
@@ -527,11 +669,16 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
   if (total > (int64_t(1) << 30)) return SRT_ERR_INVALID;
   a.total = static_cast<int32_t>(total);
   const int64_t RBR = static_cast<int64_t>(a.RB) * kRowsPerBlock;
-  a.part_o = static_cast<float*>(scratch);
-  a.part_ml = need ? static_cast<float*>(scratch) + static_cast<int64_t>(B) * Hkv * a.S * RBR * d : nullptr;
+  const size_t pbytes = plan_bytes(total);
+  a.plan = static_cast<int32_t*>(scratch);
+  a.part_o = a.S > 1 ? reinterpret_cast<float*>(static_cast<uint8_t*>(scratch) + pbytes) : nullptr;
+  a.part_ml = a.S > 1 ? a.part_o + static_cast<int64_t>(B) * Hkv * a.S * RBR * d : nullptr;
 
-  const unsigned grid = static_cast<unsigned>((total + kXcds - 1) / kXcds * kXcds);
+  const int cus = cu_count();
+  if (cus <= 0) return SRT_ERR_HIP;
+  const unsigned grid = static_cast<unsigned>(std::min<int64_t>(total, cus));
   hipStream_t s = as_stream(stream);
+  tree_attn_plan_kernel<<<1, 1024, 0, s>>>(a);
   if (d == 128) {
     tree_attn_kernel<128><<<grid, kThreads, 0, s>>>(a);
   } else {

@@ -43,10 +43,11 @@ def test_workspace_bytes_host_only():
 
 
 def test_scratch_bytes():
-    # one split: no scratch
-    assert S.srt_tree_attn_scratch_bytes(4, 8, 4, 1, 64, 16, 40) == 0
+    # one split: only the work list (header + 2 int32 per item), 256-byte rounded
+    one = S.srt_tree_attn_scratch_bytes(4, 8, 4, 1, 64, 16, 40)
+    assert one >= (64 + 2 * 4) * 4 and one % 256 == 0 and one < 4096
     n = S.srt_tree_attn_scratch_bytes(256, 64, 28, 4, 128, 16, 2052)
-    assert n > 0 and n % 4 == 0
+    assert n > one and n % 4 == 0
     assert S.srt_tree_attn_scratch_bytes(4, 8, 5, 2, 64, 16, 40) == 0  # Hq % Hkv != 0
 
 
