@@ -168,8 +168,8 @@ int srt_draft(const void* ws, int32_t B, const int32_t* prompt_ids, const int32_
  * call builds for its own kernels, plus split-context partial results when
  * a context can exceed one 4096-key split.  Owned by the caller; contents
  * are overwritten; calls that share a scratch buffer must not overlap.
- * Unsupported (SRT_ERR_UNSUPPORTED): Hkv > 255, max_pages * page beyond
- * 4095 splits of 4096 keys, or N * Hq / Hkv / 256 > 2046.
+ * Unsupported (SRT_ERR_UNSUPPORTED): B > 65535, Hkv > 255, max_pages *
+ * page beyond 4095 splits of 8192 keys, or N * Hq / Hkv / 256 > 2046.
  * ---------------------------------------------------------------------- */
 size_t srt_tree_attn_scratch_bytes(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d,
                                    int32_t page, int32_t max_pages);

@@ -62,7 +62,7 @@ constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
 constexpr int kTile = 64;                  // keys per tile
 constexpr int kSubRows = kTile / kWaves;   // keys of each tile one wave stages
 constexpr int kMaxN = 256;                 // tree rows
-constexpr int kChunk = 4096;               // keys per split
+constexpr int kChunk = 8192;               // keys per split
 
 struct AttnArgs {
   const uint16_t* q;
@@ -75,7 +75,9 @@ struct AttnArgs {
   uint16_t* out;
   float* part_o;
   float* part_ml;
-  int32_t* plan;  // work list built by the plan kernel
+  int32_t* plan;  // work lists built by the plan kernel
+  int64_t combine_at;  // offset (int32 elements) of the combine list in plan
+  int32_t max_units;   // capacity of the combine list
   int32_t B, N, Hq, Hkv, G, page, page_shift, max_pages;
   int64_t num_pages;
   float scale_log2;
@@ -86,6 +88,10 @@ struct AttnArgs {
 // then item i at plan[kPlanHeader + 2 i] = sequence, [.. + 1] = KV head |
 // split << 8 | row block << 20.  Items are ordered by decreasing cost
 // (tiles, then active waves) so that the longest ones start first.
+// plan[2] = number of combine units; unit u (8 rows of one sequence and KV
+// head whose context spans several splits) at plan[a.combine_at + u] =
+// sequence | KV head << 16 (the host rejects B > 65535) and the 8-row group
+// at plan[a.combine_at + a.max_units + u].
 constexpr int kPlanHeader = 64;
 constexpr int kPlanKeys = (kChunk / kTile) * kWaves;  // (tiles, waves) classes
 
@@ -257,15 +263,20 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   const int v_st = st_row * Sh::VSTRIDE + (lane % CPR) * 16;
 
   // Page ids of this wave's sub-block of every tile of the split, one tile
-  // per lane (a split has exactly 64 tiles), fetched once; the loop reads
-  // them with v_readlane and touches no block-table memory.
-  static_assert(kChunk / kTile == SRT_WAVE, "one lane per tile of a split");
-  int pg_lane;
-  {
-    const int p0 = k_begin + kTile * lane + kSubRows * w;
-    pg_lane = p0 < k_end ? a.bt[bt_row + (p0 >> pshift)] : -1;
+  // per lane and register (a split has 128 tiles), fetched once; the loop
+  // reads them with v_readlane and touches no block-table memory.
+  static_assert(kChunk / kTile == 2 * SRT_WAVE, "two registers of page ids per split");
+  int pg_lane[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int p0 = k_begin + kTile * (SRT_WAVE * j + lane) + kSubRows * w;
+    pg_lane[j] = p0 < k_end ? a.bt[bt_row + (p0 >> pshift)] : -1;
   }
-  auto page_of = [&](int it) { return it < ntiles ? __builtin_amdgcn_readlane(pg_lane, it) : -1; };
+  auto page_of = [&](int it) {
+    if (it >= ntiles) return -1;
+    return it < SRT_WAVE ? __builtin_amdgcn_readlane(pg_lane[0], it)
+                         : __builtin_amdgcn_readlane(pg_lane[1], it - SRT_WAVE);
+  };
   uint4 kreg[kLoadsPerWave], vreg[kLoadsPerWave];
   auto load_sub = [&](const uint16_t* base, int t0, int pg, uint4 (&r)[kLoadsPerWave]) {
     const int p0 = t0 + kSubRows * w;
@@ -531,6 +542,7 @@ __global__ __launch_bounds__(1024) void tree_attn_plan_kernel(AttnArgs a) {
   for (int b = tid; b < a.B; b += 1024)
     classes(b, [&](int key, int, int ns, int) { atomicAdd(&cnt[key], ns * a.Hkv); });
   __syncthreads();
+  __shared__ int32_t ncomb;
   if (tid == 0) {
     int run = 0;
     for (int k = 0; k < kPlanKeys; ++k) {
@@ -539,8 +551,23 @@ __global__ __launch_bounds__(1024) void tree_attn_plan_kernel(AttnArgs a) {
     }
     a.plan[0] = run;
     a.plan[1] = 0;
+    ncomb = 0;
   }
   __syncthreads();
+  // combine units: 8-row groups of every (sequence, KV head) with several splits
+  for (int b = tid; b < a.B; b += 1024) {
+    const SeqInfo si = seq_info(a, b);
+    if (si.total <= kChunk) continue;
+    const int groups = (si.n * a.G + 7) / 8;
+    int u = atomicAdd(&ncomb, groups * a.Hkv);
+    for (int g = 0; g < a.Hkv; ++g)
+      for (int r8 = 0; r8 < groups; ++r8, ++u) {
+        a.plan[a.combine_at + u] = b | (g << 16);
+        a.plan[a.combine_at + a.max_units + u] = r8;
+      }
+  }
+  __syncthreads();
+  if (tid == 0) a.plan[2] = ncomb;
   for (int b = tid; b < a.B; b += 1024)
     classes(b, [&](int key, int s0, int ns, int rb) {
       int pos = off[key] + atomicAdd(&fill[key], ns * a.Hkv);
@@ -552,44 +579,53 @@ __global__ __launch_bounds__(1024) void tree_attn_plan_kernel(AttnArgs a) {
     });
 }
 
-// Merges the split partials of sequences that needed more than one split.
-// One wave per output row (b, node, head).
+// Merges the split partials of sequences that needed more than one split:
+// out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s with M = max_s m_s (m
+// in log2 units).  Persistent workgroups stride over the combine units of
+// the plan; a unit is 8 rows, one thread per row and four head dims, so
+// partial reads are 16-byte coalesced.  The splits are folded with a
+// running maximum, so the loads of different splits are independent.
 template <int D>
 __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
-  const int wave = blockIdx.x * 4 + threadIdx.x / SRT_WAVE;
-  const int lane = threadIdx.x % SRT_WAVE;
-  const int per_seq = a.N * a.Hq;
-  if (wave >= a.B * per_seq) return;
-  const int b = wave / per_seq;
-  const int node = (wave % per_seq) / a.Hq;
-  const int h = wave % a.Hq;
-  const SeqInfo si = seq_info(a, b);
-  if (node >= si.n) return;
-  const int nsplit = (si.total + kChunk - 1) / kChunk;
-  if (nsplit <= 1) return;
-  const int g = h / a.G;
-  const int r = node * a.G + h % a.G;
+  constexpr int Q = D / 4;
+  constexpr int kRowsPerUnit = 256 / Q;
+  static_assert(kRowsPerUnit * Q == 256 && kRowsPerUnit >= 8, "unit shape");
+  const int n_units = a.plan[2];
   const int RBR = a.RB * kRowsPerBlock;
-  const int64_t base = (static_cast<int64_t>(b) * a.Hkv + g) * a.S * RBR + r;
-  float M = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, a.part_ml[2 * (base + static_cast<int64_t>(s) * RBR)]);
-  constexpr int PER = D / SRT_WAVE;
-  float num[PER];
-#pragma unroll
-  for (int i = 0; i < PER; ++i) num[i] = 0.f;
-  float den = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const int64_t prow = base + static_cast<int64_t>(s) * RBR;
-    const float ms = a.part_ml[2 * prow];
-    const float wgt = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M);
-    den += wgt * a.part_ml[2 * prow + 1];
-#pragma unroll
-    for (int i = 0; i < PER; ++i) num[i] += wgt * a.part_o[prow * D + lane + SRT_WAVE * i];
+  for (int u = blockIdx.x; u < n_units; u += gridDim.x) {
+    const int bg = a.plan[a.combine_at + u];
+    const int b = bg & 0xffff, g = bg >> 16;
+    const SeqInfo si = seq_info(a, b);
+    const int nsplit = (si.total + kChunk - 1) / kChunk;
+    const int rows = si.n * a.G;
+    for (int sub = threadIdx.x; sub < 8 * Q; sub += 256) {
+      const int r = a.plan[a.combine_at + a.max_units + u] * 8 + sub / Q, q = sub % Q;
+      if (r >= rows) continue;
+      const int64_t base = (static_cast<int64_t>(b) * a.Hkv + g) * a.S * RBR + r;
+      float M = -INFINITY, den = 0.f;
+      f32x4 num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+      for (int s = 0; s < nsplit; ++s) {
+        const int64_t prow = base + static_cast<int64_t>(s) * RBR;
+        const float ms = a.part_ml[2 * prow];
+        const float ls = a.part_ml[2 * prow + 1];
+        const f32x4 os = *reinterpret_cast<const f32x4*>(a.part_o + prow * D + 4 * q);
+        if (ms == -INFINITY) continue;
+        const float mn = fmaxf(M, ms);
+        const float c_old = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - mn);
+        const float c_new = __builtin_amdgcn_exp2f(ms - mn);
+        den = den * c_old + ls * c_new;
+        num = num * c_old + os * c_new;
+        M = mn;
+      }
+      const float inv = den > 0.f ? 1.f / den : 0.f;
+      const int node = r / a.G, h = g * a.G + r % a.G;
+      uint16_t* op = a.out + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + h) * D + 4 * q;
+      const uint32_t x0 = to_bf16_bits(num[0] * inv) | (uint32_t(to_bf16_bits(num[1] * inv)) << 16);
+      const uint32_t x1 = to_bf16_bits(num[2] * inv) | (uint32_t(to_bf16_bits(num[3] * inv)) << 16);
+      *reinterpret_cast<uint2*>(op) = make_uint2(x0, x1);
+    }
   }
-  const float inv = den > 0.f ? 1.f / den : 0.f;
-  uint16_t* op = a.out + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + h) * D;
-#pragma unroll
-  for (int i = 0; i < PER; ++i) op[lane + SRT_WAVE * i] = to_bf16_bits(num[i] * inv);
 }
 
 int splits_for(int32_t page, int32_t max_pages) {
@@ -597,8 +633,16 @@ int splits_for(int32_t page, int32_t max_pages) {
   return static_cast<int>((cap + kChunk - 1) / kChunk);
 }
 
-// Bytes of the work list for at most B * Hkv * S * RB items, rounded to 256.
-size_t plan_bytes(int64_t items) { return ((kPlanHeader + 2 * items) * sizeof(int32_t) + 255) / 256 * 256; }
+// Combine units (8-row groups) needed at most.
+int64_t max_combine_units(int32_t B, int32_t N, int32_t G, int32_t Hkv) {
+  return static_cast<int64_t>(B) * Hkv * ((static_cast<int64_t>(N) * G + 7) / 8);
+}
+
+// Bytes of the work lists for at most `items` items and `units` combine
+// units, rounded to 256.
+size_t plan_bytes(int64_t items, int64_t units) {
+  return ((kPlanHeader + 2 * items + 2 * units) * sizeof(int32_t) + 255) / 256 * 256;
+}
 
 int cu_count() {
   static int cached[64] = {0};
@@ -619,7 +663,7 @@ extern "C" size_t srt_tree_attn_scratch_bytes(int32_t B, int32_t N, int32_t Hq, 
   const int S = splits_for(page, max_pages);
   const int G = Hq / Hkv;
   const int64_t RB = (N * G + kRowsPerBlock - 1) / kRowsPerBlock;
-  const size_t plan = plan_bytes(static_cast<int64_t>(B) * Hkv * S * RB);
+  const size_t plan = plan_bytes(static_cast<int64_t>(B) * Hkv * S * RB, max_combine_units(B, N, G, Hkv));
   if (S <= 1) return plan;
   return plan + static_cast<size_t>(B) * Hkv * S * RB * kRowsPerBlock * (d + 2) * sizeof(float);
 }
@@ -634,8 +678,10 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
   if (!(scale == scale)) return SRT_ERR_INVALID;
   if (d != 64 && d != 128) return SRT_ERR_UNSUPPORTED;
   if (page < 16 || (page & (page - 1))) return SRT_ERR_UNSUPPORTED;
-  // work-list packing: KV head < 256, split < 4096, row block < 2048
-  if (Hkv > 255 || splits_for(page, max_pages) > 4095 || (N * (Hq / Hkv)) / kRowsPerBlock > 2046)
+  // work-list packing: sequence < 65536, KV head < 256, split < 4096,
+  // row block < 2048, combine units < 2^31
+  if (B > 65535 || Hkv > 255 || splits_for(page, max_pages) > 4095 || (N * (Hq / Hkv)) / kRowsPerBlock > 2046 ||
+      max_combine_units(B, N, Hq / Hkv, Hkv) > (int64_t(1) << 30))
     return SRT_ERR_UNSUPPORTED;
   if (B == 0) return SRT_OK;
   if (!q || !k_cache || !v_cache || !block_table || !ctx_len || !tree_parent || !n_nodes || !out)
@@ -669,8 +715,11 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
   if (total > (int64_t(1) << 30)) return SRT_ERR_INVALID;
   a.total = static_cast<int32_t>(total);
   const int64_t RBR = static_cast<int64_t>(a.RB) * kRowsPerBlock;
-  const size_t pbytes = plan_bytes(total);
+  const int64_t units = max_combine_units(B, N, a.G, Hkv);
+  const size_t pbytes = plan_bytes(total, units);
   a.plan = static_cast<int32_t*>(scratch);
+  a.combine_at = kPlanHeader + 2 * total;
+  a.max_units = static_cast<int32_t>(units);
   a.part_o = a.S > 1 ? reinterpret_cast<float*>(static_cast<uint8_t*>(scratch) + pbytes) : nullptr;
   a.part_ml = a.S > 1 ? a.part_o + static_cast<int64_t>(B) * Hkv * a.S * RBR * d : nullptr;
 
@@ -685,8 +734,7 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
     tree_attn_kernel<64><<<grid, kThreads, 0, s>>>(a);
   }
   if (a.S > 1) {
-    const int64_t rows = static_cast<int64_t>(B) * N * Hq;
-    const unsigned cgrid = static_cast<unsigned>((rows + 3) / 4);
+    const unsigned cgrid = static_cast<unsigned>(std::min<int64_t>(units, 4 * cus));
     if (d == 128) {
       tree_attn_combine_kernel<128><<<cgrid, 256, 0, s>>>(a);
     } else {

@@ -76,10 +76,18 @@ def test_shapes_ragged(d, hq, hkv):
 
 
 def test_split_contexts_and_combine():
-    # contexts longer than one split (4096 keys) exercise the partial + combine path
+    # contexts longer than one split (8192 keys) exercise the partial + combine
+    # path; lengths sit on and around split and tile boundaries
     say("attn: split contexts")
-    ctx = [4095 - 7, 4096 - 64, 4096, 5000, 9000, 12345, 100]
+    ctx = [4088, 8192 - 64 - 7, 8192 - 64, 8192, 9000, 12345, 16384 - 30, 25000, 100]
     c = Case(11, len(ctx), 64, 28, 4, 128, ctx)
+    c.check(c.run())
+
+
+def test_split_contexts_d64():
+    say("attn: split contexts, d=64")
+    ctx = [8200, 17000, 3]
+    c = Case(29, len(ctx), 32, 14, 2, 64, ctx)
     c.check(c.run())
 
 
