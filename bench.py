@@ -199,7 +199,7 @@ def main():
         roof = {"bound": "hbm", "achieved": nbytes / t_attn / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = counter_traffic()
-    roof["kernel"] = "srt_tree_attn (tree_attn_kernel + tree_attn_combine_kernel)"
+    roof["kernel"] = "srt_tree_attn (tree_attn_plan_kernel + tree_attn_kernel + tree_attn_combine_kernel)"
     roof["algorithmic_bytes"] = nbytes
     roof["algorithmic_flops"] = flops
     roof["launch_ms"] = part_ms["attention"]
