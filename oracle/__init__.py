@@ -22,8 +22,11 @@ method computes, written from the paper (SRT, arXiv 2601.09083):
                    "Speculative Decoding").
 * ``accept``    -- lossless acceptance up to the first mismatch, plus the
                    target's own token at the mismatch (Section 1; Section 3).
+* ``commit``    -- the accepted path's key/value vectors moved into the
+                   committed positions and the context advanced (Section 3,
+                   classic speculative decoding; Appendix C).
 
 Pins (tests marked ``not gpu``) tie each function to closed forms, brute
 force, library routines and invariants; see ``tests/test_oracle_*.py``.
 """
-from . import accept, attention, draft, trie  # noqa: F401
+from . import accept, attention, commit, draft, trie  # noqa: F401
