@@ -5,7 +5,9 @@ A step is one pass of the whole hot path over one batch: srt_draft (draft
 trees from the per-prompt caches) -> srt_tree_attn (tree-masked attention of
 every node over its paged context) -> srt_accept (acceptance walk with T=1
 Gumbel sampling) -> srt_trie_insert (emitted tokens appended to each
-sequence's stream).  Inputs are resident in HBM before timing starts.
+sequence's stream) -> srt_commit (accepted nodes' K/V moved into place,
+contexts and draft tails advanced), so consecutive steps form a real decode
+loop.  Inputs are resident in HBM before timing starts.
 
 Default workload: the Qwen2.5-7B-shaped layer (256 sequences, 28 query / 4
 KV heads, head_dim 128, log-normal contexts with median 4k and max 32k,
@@ -36,19 +38,17 @@ COUNTERS = os.path.join(ROOT, "profiles", "tree_attn_qwen7b_counters.json")
 ATTN_SRC = os.path.join(ROOT, "paper_2601_09083_amd", "csrc", "tree_attn.hip")
 
 
-def attn_work(cfg, ctx_len, tree_np):
+def attn_work(cfg, ctx_len, n_nodes, tree_depth):
     """Algorithmic bytes and FLOPs of one tree-attention launch: every K/V
     position of every sequence read once (context + tree), Q read once, O
     written once; 4*d FLOPs per (query row, visible key)."""
-    n = tree_np["n_nodes"].astype(np.int64)
+    n = n_nodes.astype(np.int64)
     L = ctx_len.astype(np.int64)
     d, hq, hkv = cfg.head_dim, cfg.hq, cfg.hkv
     kv_bytes = int(((L + n) * hkv * d * 2 * 2).sum())
     qo_bytes = int((n * hq * d * 2 * 2).sum())
-    depth = tree_np["tree_depth"]
-    vis = 0
-    for b in range(len(n)):
-        vis += int(n[b]) * int(L[b]) + int((depth[b, : n[b]] + 1).sum())
+    valid = np.arange(tree_depth.shape[1])[None, :] < n[:, None]
+    vis = int((n * L).sum()) + int(np.where(valid, tree_depth.astype(np.int64) + 1, 0).sum())
     flops = 4 * d * hq * vis
     return kv_bytes + qo_bytes, flops
 
@@ -74,11 +74,13 @@ def counter_traffic():
 def cpu_baseline(st, tree_np, budget_s: float):
     """The oracle, as it stands, on a bounded sample of the same workload:
     per sequence the draft (from the prompt's stream index), fp64 tree
-    attention, the acceptance walk and the online insert; 1 thread."""
+    attention, the acceptance walk, the online insert and the commit of the
+    accepted path; 1 thread."""
     from threadpoolctl import threadpool_limits
 
     from oracle import accept as AC
     from oracle import attention as AT
+    from oracle import commit as CM
     from oracle import draft as DR
     from oracle import trie as TR
 
@@ -109,6 +111,9 @@ def cpu_baseline(st, tree_np, budget_s: float):
             k, out, nodes = AC.accept(lambda u: logits[u], (lambda s: noise[s]) if noise is not None else None,
                                       1.0, tok, par, n, cfg.max_depth)
             TR.insert_counts({}, tw.seqs[b][-cfg.trie_depth:], out, cfg.trie_depth)
+            for cache in (kc, vc):
+                CM.commit_kv(AT.gather_positions(cache, np.arange(npg), L + n, cfg.page), L, k, nodes)
+            CM.commit_tail(tails[b], int(ts[b]), out)
             t_total += time.perf_counter() - t0
             tok_total += n
             seqs += 1
@@ -116,7 +121,7 @@ def cpu_baseline(st, tree_np, budget_s: float):
                 break
     return {"value": tok_total / t_total, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"{seqs} of {tw.batch} sequences of the {cfg.name} workload, one step each "
-                      f"(draft + fp64 tree attention + acceptance + insert), {t_total:.1f} s on 1 thread"}
+                      f"(draft + fp64 tree attention + acceptance + insert + commit), {t_total:.1f} s on 1 thread"}
 
 
 def main():
@@ -155,7 +160,8 @@ def main():
         return
     cfg = W.CONFIGS[args.config]
     t_setup = time.perf_counter()
-    st = VerifyState.build(cfg, steps_headroom=args.steps + args.warmup + 4)
+    n_steps = args.steps + args.warmup + 4
+    st = VerifyState.build(cfg, steps_headroom=n_steps, kv_headroom=n_steps * (cfg.max_depth + 1))
     st.draft()
     st.make_logits(sampled=not args.greedy)
     torch.cuda.synchronize()
@@ -166,12 +172,18 @@ def main():
         st.step()
     torch.cuda.synchronize()
 
-    parts = ("draft", "attention", "accept", "insert")
+    parts = ("draft", "attention", "accept", "insert", "commit")
     ev = {p: [] for p in parts}
     stream = torch.cuda.current_stream()
+    B = st.tokens.batch
+    # per-step record of what each attention launch saw (context lengths
+    # and tree sizes / depths), copied on the device after the launch
+    rec_len = torch.empty((args.steps, 2, B), dtype=torch.int32, device=st.attn_len.device)
+    rec_depth = torch.empty((args.steps, B, cfg.n_nodes), dtype=torch.int32, device=st.attn_len.device)
+    rec_emit = torch.empty((args.steps, B), dtype=torch.int32, device=st.attn_len.device)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for k in range(args.steps):
         for p in parts:
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
@@ -179,18 +191,26 @@ def main():
             getattr(st, p)()
             e1.record(stream)
             ev[p].append((e0, e1))
+            if p == "attention":
+                rec_len[k, 0].copy_(st.attn_len)
+                rec_len[k, 1].copy_(st.tree["n_nodes"])
+                rec_depth[k].copy_(st.tree["tree_depth"])
+            elif p == "accept":
+                rec_emit[k].copy_(st.acc["n_emitted"])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     part_ms = {p: float(np.mean([a.elapsed_time(b) for a, b in ev[p]])) for p in parts}
 
+    rl, rd, re_ = rec_len.cpu().numpy(), rec_depth.cpu().numpy(), rec_emit.cpu().numpy()
     tree_np = {k: v.cpu().numpy() for k, v in st.tree.items()}
-    acc_np = {k: v.cpu().numpy() for k, v in st.acc.items()}
-    n_tree = int(tree_np["n_nodes"].sum())
-    n_emit = int(acc_np["n_emitted"].sum())
+    n_tree = int(rl[:, 1].sum())
+    n_emit = int(re_.sum())
     ms_step = wall * 1e3 / args.steps
-    value = n_tree / (ms_step / 1e3)
+    value = n_tree / args.steps / (ms_step / 1e3)
 
-    nbytes, flops = attn_work(cfg, st.tokens.ctx_len, tree_np)
+    work = [attn_work(cfg, rl[k, 0], rl[k, 1], rd[k]) for k in range(args.steps)]
+    nbytes = float(np.mean([w[0] for w in work]))
+    flops = float(np.mean([w[1] for w in work]))
     t_attn = part_ms["attention"] / 1e3
     t_hbm, t_mfma = nbytes / (HBM_PEAK_GBPS * 1e9), flops / (BF16_PEAK_TFLOPS * 1e12)
     if t_mfma >= t_hbm:
@@ -231,9 +251,9 @@ def main():
         },
         "tree_attn_hbm": {"achieved_GBps": attn_hbm, "peak_GBps": HBM_PEAK_GBPS, "frac": attn_hbm / HBM_PEAK_GBPS},
         "parts_ms": part_ms,
-        "accepted_tokens_per_s": n_emit / (ms_step / 1e3),
-        "mean_tree_nodes": n_tree / st.tokens.batch,
-        "mean_emitted": n_emit / st.tokens.batch,
+        "accepted_tokens_per_s": n_emit / args.steps / (ms_step / 1e3),
+        "mean_tree_nodes": n_tree / args.steps / B,
+        "mean_emitted": n_emit / args.steps / B,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -10,6 +10,7 @@
  *   (caller)       -> LM head: per-node logits
  *   srt_accept     -> accepted path + bonus token
  *   srt_trie_insert-> emitted tokens appended to the sequence's stream
+ *   srt_commit     -> accepted nodes' K/V moved into place, context advanced
  *
  * Conventions shared by every entry point
  *   - Pointers are device pointers unless the comment says "host".  All
@@ -166,7 +167,7 @@ int srt_draft(const void* ws, int32_t B, const int32_t* prompt_ids, const int32_
  * scratch: device buffer, 256-byte aligned, of at least
  * srt_tree_attn_scratch_bytes(...) bytes (always > 0): the work list the
  * call builds for its own kernels, plus split-context partial results when
- * a context can exceed one 4096-key split.  Owned by the caller; contents
+ * a context can exceed one 8192-key split.  Owned by the caller; contents
  * are overwritten; calls that share a scratch buffer must not overlap.
  * Unsupported (SRT_ERR_UNSUPPORTED): B > 65535, Hkv > 255, max_pages *
  * page beyond 4095 splits of 8192 keys, or N * Hq / Hkv / 256 > 2046.
@@ -204,6 +205,38 @@ int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logit
                const float* gumbel, float inv_temperature, const int32_t* tree_tokens,
                const int32_t* tree_parent, const int32_t* n_nodes, int32_t* n_accepted,
                int32_t* out_tokens, int32_t* out_nodes, int32_t* n_emitted, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Commit of the accepted path (Section 3: the verification pass keeps the
+ * accepted tokens as classic speculative decoding does; Appendix C).
+ *
+ * The verification pass computed the key/value vectors of every tree node i
+ * at position L + i (L = ctx_len[b], the root at L).  With
+ * k = n_accepted[b] and accepted nodes c_j = out_nodes[b, j-1], j = 1..k, as
+ * returned by srt_accept (increasing tree indices, 1 <= c_j < N):
+ *   K/V at position L + j  <-  K/V at position L + c_j, every KV head;
+ *   positions <= L and > L + k are not written;
+ *   ctx_len[b] += k + 1   (root and accepted nodes become context);
+ * and, if ctx_tail is not NULL, the draft inputs advance by the k + 1
+ * emitted tokens out_tokens[b, 0..k] (accepted tokens, then the bonus
+ * token): ctx_tail[b] (right-aligned last max_match committed tokens, -1
+ * padded, as srt_draft reads it) becomes the last max_match tokens of the
+ * grown sequence and draft_len[b] += k + 1.  The bonus token is the next
+ * pass's root; its vectors are the caller's to write at the new L.
+ * Layouts: k_cache, v_cache [num_pages, Hkv, page, d] bf16 bits, 16-byte
+ * aligned, updated in place; block_table [B, max_pages] int32; ctx_len,
+ * n_accepted, draft_len [B] int32; out_tokens, out_nodes [B, Dmax+1]
+ * int32; ctx_tail [B, max_match] int32.  ctx_tail and draft_len are both
+ * NULL or both set.  k is clamped to [0, min(Dmax, N-1)]; a copy whose node
+ * index is outside [1, N) or whose page is outside the block table or the
+ * pool is skipped.  d must be a multiple of 8 up to 1024
+ * (else SRT_ERR_UNSUPPORTED).
+ * ---------------------------------------------------------------------- */
+int srt_commit(int32_t B, int32_t N, int32_t Hkv, int32_t d, int32_t page, int32_t max_pages,
+               int64_t num_pages, uint16_t* k_cache, uint16_t* v_cache, const int32_t* block_table,
+               int32_t* ctx_len, int32_t Dmax, const int32_t* n_accepted, const int32_t* out_tokens,
+               const int32_t* out_nodes, int32_t max_match, int32_t* ctx_tail, int32_t* draft_len,
+               void* stream);
 
 /* Library version string (host only). */
 const char* srt_version(void);

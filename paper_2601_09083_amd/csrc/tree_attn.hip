@@ -28,9 +28,10 @@
 //     reads of every MFMA are bank-conflict free and their addresses are one
 //     base register plus immediate offsets.
 //   * Softmax uses exp2 with scale*log2(e) folded in and a lazily raised
-//     reference maximum.  The ancestor mask is a bitset per tree node in LDS
-//     and is applied only on tiles that reach the tree positions or the end
-//     of the range.
+//     reference maximum.  The ancestor mask is a bitset per tree node in LDS;
+//     on tiles that reach the tree positions or the end of the range each
+//     row takes a 64-bit visibility window of it (two LDS words) and masks
+//     its scores bit by bit.
 //   * Long contexts are split into fixed chunks of keys so the grid has
 //     enough independent work; each split writes unnormalised partial
 //     output plus (max, sum) and a small combine kernel merges them.  A
@@ -332,20 +333,38 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   auto softmax = [&](int t0, f32x16 (&sacc)[2], bf16x8 (&pb)[4]) {
     const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
     if (need_mask) {
+      // Visibility of keys t0 .. t0+63 for this lane's row as one 64-bit
+      // window: bit x is set iff key t0 + x < k_end and it is a context key
+      // or the tree position of an ancestor-or-self of the row's node.  (If
+      // the split ends before the tree, bits of tree positions are cleared
+      // by the k_end limit, so stale bitsets are never used.)
+      const int lim = k_end - t0;
+      uint64_t vis = lim >= 64 ? ~0ull : (lim <= 0 ? 0ull : (~0ull >> (64 - lim)));
+      const int j0 = t0 - si.L;  // tree index of key t0
+      if (j0 > -kTile) {
+        uint64_t win;
+        if (j0 >= 0) {
+          const int wd = j0 >> 6, sh = j0 & 63;
+          const uint64_t lo = wd < 4 ? anc[node][wd] : 0ull;
+          const uint64_t hi = wd + 1 < 4 ? anc[node][wd + 1] : 0ull;
+          win = sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
+        } else {
+          const int sh = -j0;  // 1..63 context keys lead the window
+          win = (anc[node][0] << sh) | (~0ull >> (64 - sh));
+        }
+        vis &= win;
+      }
+      // lane half h holds keys 32 kb + 8 (r/4) + 4 h + r%4
+      const uint64_t vh = vis >> (4 * h);
+      const uint32_t v0 = static_cast<uint32_t>(vh), v1 = static_cast<uint32_t>(vh >> 32);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        f32x16 t = sacc[kb];
+        const uint32_t vw = kb ? v1 : v0;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int pos = t0 + 32 * kb + 8 * (r / 4) + 4 * h + r % 4;
-          bool vis = pos < k_end;
-          if (vis && pos >= si.L) {
-            const int j = pos - si.L;
-            vis = (anc[node][j >> 6] >> (j & 63)) & 1ull;
-          }
-          t[r] = vis ? t[r] : -INFINITY;
+          const int x = 8 * (r / 4) + r % 4;
+          sacc[kb][r] = ((vw >> x) & 1u) ? sacc[kb][r] : -INFINITY;
         }
-        sacc[kb] = t;
       }
     }
     // (maximum, not fmaxf: no NaN-quieting of every operand; scores are
@@ -516,40 +535,53 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
 }
 
 // Builds the work list: one item per (sequence, KV head, split, row block)
-// that has work, counting-sorted by decreasing (tiles, active waves).  One
-// workgroup; also resets the hand-out counter.
+// that has work, counting-sorted by decreasing (tiles, active waves of the
+// first row block).  The row blocks of one (sequence, KV head, split) are
+// listed next to each other, so workgroups that take them start at about
+// the same time and the second stream of the same K/V tiles is served by
+// the caches.  One workgroup; also resets the hand-out counter.
 __global__ __launch_bounds__(1024) void tree_attn_plan_kernel(AttnArgs a) {
   __shared__ int32_t cnt[kPlanKeys], off[kPlanKeys], fill[kPlanKeys];
+  __shared__ int32_t wsum[1024 / SRT_WAVE];
   const int tid = threadIdx.x;
   for (int k = tid; k < kPlanKeys; k += 1024) {
     cnt[k] = 0;
     fill[k] = 0;
   }
   __syncthreads();
-  // Visits the item classes of sequence b: f(key, first split, splits).
+  // Visits the item classes of sequence b: f(key, first split, splits,
+  // row blocks).
   auto classes = [&](int b, auto&& f) {
     const SeqInfo si = seq_info(a, b);
     const int rows = si.n * a.G;
     const int rbs = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
     const int full = si.total / kChunk;
     const int tail = si.total - full * kChunk;
-    for (int rb = 0; rb < rbs; ++rb) {
-      const int waves = min(kWaves, (rows - rb * kRowsPerBlock + kRowsPerWave - 1) / kRowsPerWave);
-      if (full > 0) f(plan_key(kChunk / kTile, waves), 0, full, rb);
-      if (tail > 0) f(plan_key((tail + kTile - 1) / kTile, waves), full, 1, rb);
-    }
+    const int waves = min(kWaves, (rows + kRowsPerWave - 1) / kRowsPerWave);
+    if (full > 0) f(plan_key(kChunk / kTile, waves), 0, full, rbs);
+    if (tail > 0) f(plan_key((tail + kTile - 1) / kTile, waves), full, 1, rbs);
   };
   for (int b = tid; b < a.B; b += 1024)
-    classes(b, [&](int key, int, int ns, int) { atomicAdd(&cnt[key], ns * a.Hkv); });
+    classes(b, [&](int key, int, int ns, int rbs) { atomicAdd(&cnt[key], ns * a.Hkv * rbs); });
   __syncthreads();
+  // Exclusive prefix sum of the class counts (one class per thread).
+  static_assert(kPlanKeys <= 1024, "one class per thread");
+  const int lane = tid % SRT_WAVE, wv = tid / SRT_WAVE;
+  const int mine = tid < kPlanKeys ? cnt[tid] : 0;
+  int incl = mine;
+#pragma unroll
+  for (int d = 1; d < SRT_WAVE; d <<= 1) {
+    const int y = __shfl_up(incl, d, SRT_WAVE);
+    if (lane >= d) incl += y;
+  }
+  if (lane == SRT_WAVE - 1) wsum[wv] = incl;
+  __syncthreads();
+  int before = 0;
+  for (int j = 0; j < wv; ++j) before += wsum[j];
+  if (tid < kPlanKeys) off[tid] = before + incl - mine;
   __shared__ int32_t ncomb;
-  if (tid == 0) {
-    int run = 0;
-    for (int k = 0; k < kPlanKeys; ++k) {
-      off[k] = run;
-      run += cnt[k];
-    }
-    a.plan[0] = run;
+  if (tid == 1023) {
+    a.plan[0] = before + incl;  // all classes
     a.plan[1] = 0;
     ncomb = 0;
   }
@@ -569,13 +601,14 @@ __global__ __launch_bounds__(1024) void tree_attn_plan_kernel(AttnArgs a) {
   __syncthreads();
   if (tid == 0) a.plan[2] = ncomb;
   for (int b = tid; b < a.B; b += 1024)
-    classes(b, [&](int key, int s0, int ns, int rb) {
-      int pos = off[key] + atomicAdd(&fill[key], ns * a.Hkv);
+    classes(b, [&](int key, int s0, int ns, int rbs) {
+      int pos = off[key] + atomicAdd(&fill[key], ns * a.Hkv * rbs);
       for (int s = s0; s < s0 + ns; ++s)
-        for (int g = 0; g < a.Hkv; ++g, ++pos) {
-          a.plan[kPlanHeader + 2 * pos] = b;
-          a.plan[kPlanHeader + 2 * pos + 1] = g | (s << 8) | (rb << 20);
-        }
+        for (int g = 0; g < a.Hkv; ++g)
+          for (int rb = 0; rb < rbs; ++rb, ++pos) {
+            a.plan[kPlanHeader + 2 * pos] = b;
+            a.plan[kPlanHeader + 2 * pos + 1] = g | (s << 8) | (rb << 20);
+          }
     });
 }
 

@@ -1,8 +1,10 @@
 """One SRT verification step on the GPU, assembled from the libsrt calls.
 
 ``VerifyState`` owns the device buffers of one workload (per-prompt caches,
-paged KV cache, queries, logits, noise) and runs the four calls of a step:
-``srt_draft`` -> ``srt_tree_attn`` -> ``srt_accept`` -> ``srt_trie_insert``.
+paged KV cache, queries, logits, noise) and runs the calls of a step:
+``srt_draft`` -> ``srt_tree_attn`` -> ``srt_accept`` -> ``srt_trie_insert``
+-> ``srt_commit`` (the accepted path becomes context, so the next step drafts
+and attends from the grown sequence).
 Only buffer management and argument passing happen here; every step of the
 path runs in the HIP kernels of libsrt.
 """
@@ -122,7 +124,7 @@ class VerifyState:
     # ---- set-up ---------------------------------------------------------
     @classmethod
     def build(cls, cfg: W.Config, device="cuda", tokens: Optional[W.TokenWorkload] = None,
-              steps_headroom: int = 64, with_seqs: bool = True):
+              steps_headroom: int = 64, with_seqs: bool = True, kv_headroom: int = 0):
         tw = W.make_tokens(cfg) if tokens is None else tokens
         B = tw.batch
         streams, sp = [], []
@@ -143,7 +145,7 @@ class VerifyState:
         ids = caches.new_streams(len(streams))
         caches.insert(sp, ids, streams)
         seq_stream = ids[n_prior:] if with_seqs else caches.new_streams(B)
-        q, k, v, bt, P = W.make_kv(cfg, tw.ctx_len, device=device)
+        q, k, v, bt, P = W.make_kv(cfg, tw.ctx_len, device=device, headroom=kv_headroom)
         st = cls(cfg=cfg, tokens=tw, caches=caches, seq_stream=seq_stream.astype(np.int32), device=device,
                  prompt_ids=_dev(tw.seq_prompt, device), ctx_tail=_dev(tw.ctx_tail(), device),
                  draft_len=_dev(tw.draft_len(), device), attn_len=_dev(tw.ctx_len, device), q=q, k_cache=k,
@@ -187,8 +189,14 @@ class VerifyState:
         srt.srt_trie_insert(self.caches.ws, self.prompt_ids, self.seq_stream_dev, self.acc["out_tokens"],
                             self.acc["n_emitted"])
 
+    def commit(self):
+        srt.srt_commit(self.k_cache, self.v_cache, self.block_table, self.attn_len, self.acc["n_accepted"],
+                       self.acc["out_tokens"], self.acc["out_nodes"], self.cfg.n_nodes, ctx_tail=self.ctx_tail,
+                       draft_len=self.draft_len)
+
     def step(self, inv_temperature: float = 1.0):
         self.draft()
         self.attention()
         self.accept(inv_temperature)
         self.insert()
+        self.commit()

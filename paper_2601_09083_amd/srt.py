@@ -25,7 +25,7 @@ _NAMES = {SRT_ERR_INVALID: "SRT_ERR_INVALID", SRT_ERR_CAPACITY: "SRT_ERR_CAPACIT
 # Every symbol include/srt.h declares.
 EXPORTS = ("srt_trie_workspace_bytes", "srt_trie_init", "srt_trie_insert", "srt_trie_reset_streams",
            "srt_trie_status", "srt_trie_export", "srt_draft", "srt_tree_attn_scratch_bytes",
-           "srt_tree_attn", "srt_accept", "srt_version")
+           "srt_tree_attn", "srt_accept", "srt_commit", "srt_version")
 
 
 class SrtError(RuntimeError):
@@ -68,6 +68,7 @@ def lib() -> ctypes.CDLL:
             "srt_tree_attn_scratch_bytes": (_SZ, [_I32] * 7),
             "srt_tree_attn": (ctypes.c_int, [_I32] * 7 + [_I64] + [_P] * 7 + [ctypes.c_float, _P, _P, _SZ, _P]),
             "srt_accept": (ctypes.c_int, [_I32] * 4 + [_P, _P, ctypes.c_float] + [_P] * 8),
+            "srt_commit": (ctypes.c_int, [_I32] * 6 + [_I64] + [_P] * 4 + [_I32] + [_P] * 3 + [_I32, _P, _P, _P]),
             "srt_version": (ctypes.c_char_p, []),
         }
         for name, (res, args) in sig.items():
@@ -224,6 +225,27 @@ def srt_accept(logits, gumbel, inv_temperature: float, tree_tokens, tree_parent,
         _ptr(out["n_accepted"], torch.int32), _ptr(out["out_tokens"], torch.int32),
         _ptr(out["out_nodes"], torch.int32), _ptr(out.get("n_emitted"), torch.int32), _stream(stream)))
     return out
+
+
+# --------------------------------------------------------------------------- commit
+
+def srt_commit(k_cache, v_cache, block_table, ctx_len, n_accepted, out_tokens, out_nodes, n_nodes_max: int,
+               ctx_tail=None, draft_len=None, stream=None):
+    """Moves the accepted nodes' K/V into place and advances ctx_len (and, if
+    given, ctx_tail [B, Qmax] / draft_len [B]) in place."""
+    B = int(ctx_len.numel())
+    P, Hkv, page, d = k_cache.shape
+    if v_cache.shape != k_cache.shape:
+        raise ValueError("cache shape mismatch")
+    dmax = int(out_tokens.shape[1]) - 1
+    qmax = int(ctx_tail.shape[1]) if ctx_tail is not None else 0
+    _check("srt_commit", lib().srt_commit(
+        B, int(n_nodes_max), Hkv, d, page, int(block_table.shape[1]), P,
+        _ptr(k_cache, torch.bfloat16, "k_cache"), _ptr(v_cache, torch.bfloat16, "v_cache"),
+        _ptr(block_table, torch.int32, "block_table"), _ptr(ctx_len, torch.int32, "ctx_len"), dmax,
+        _ptr(n_accepted, torch.int32, "n_accepted"), _ptr(out_tokens, torch.int32, "out_tokens"),
+        _ptr(out_nodes, torch.int32, "out_nodes"), qmax, _ptr(ctx_tail, torch.int32, "ctx_tail"),
+        _ptr(draft_len, torch.int32, "draft_len"), _stream(stream)))
 
 
 def srt_version() -> str:

@@ -270,8 +270,9 @@ def _gen(device, seed: int):
 
 
 def make_kv(cfg: Config, ctx_len: np.ndarray, device="cpu", seed: Optional[int] = None,
-            n_nodes: Optional[int] = None):
-    """Paged bf16 KV cache with room for ``n_nodes`` tree tokens per sequence.
+            n_nodes: Optional[int] = None, headroom: int = 0):
+    """Paged bf16 KV cache with room for ``n_nodes`` tree tokens per sequence,
+    plus ``headroom`` positions for contexts that grow.
 
     Returns (q [B,N,Hq,d] bf16, k_cache, v_cache [P,Hkv,page,d] bf16,
     block_table [B,max_pages] int32 (-1 padded), num_pages)."""
@@ -279,7 +280,7 @@ def make_kv(cfg: Config, ctx_len: np.ndarray, device="cpu", seed: Optional[int] 
     seed = (1000 + cfg.index) * 7 + 1 if seed is None else seed
     N = cfg.n_nodes if n_nodes is None else n_nodes
     B = int(ctx_len.shape[0])
-    pages_per = (ctx_len.astype(np.int64) + N + cfg.page - 1) // cfg.page
+    pages_per = (ctx_len.astype(np.int64) + N + headroom + cfg.page - 1) // cfg.page
     P = int(pages_per.sum())
     max_pages = int(pages_per.max())
     rng = np.random.Generator(np.random.PCG64(seed))

@@ -79,6 +79,38 @@ def test_tiny_two_steps(sampled):
 FULL = {"qwen1.5b": 3, "grpo": 2, "qwen7b": 3, "longtail": 2}
 
 
+def seq_rows(cache, bt_row, positions, page):
+    """[len(positions), Hkv, d] int16 bits of one sequence's logical positions."""
+    pos = torch.as_tensor(positions, dtype=torch.long, device=cache.device)
+    pages = bt_row.long()[pos // page]
+    return cache[pages, :, pos % page, :].view(torch.int16).cpu().numpy()
+
+
+def check_commit(st, acc, sample):
+    """srt_commit over the whole batch; the sampled sequences' tree window,
+    lengths and draft tails are compared with the oracle's commit."""
+    from oracle import commit as CM
+    c = st.cfg
+    L = st.attn_len.cpu().numpy().astype(np.int64)
+    t = st.draft_len.cpu().numpy().astype(np.int64)
+    tails = st.ctx_tail.cpu().numpy()
+    before = {b: (seq_rows(st.k_cache, st.block_table[b], np.arange(L[b], L[b] + c.n_nodes), c.page),
+                  seq_rows(st.v_cache, st.block_table[b], np.arange(L[b], L[b] + c.n_nodes), c.page)) for b in sample}
+    st.commit()
+    torch.cuda.synchronize()
+    k_acc = acc["n_accepted"]
+    assert st.attn_len.cpu().numpy().tolist() == (L + k_acc + 1).tolist()
+    assert st.draft_len.cpu().numpy().tolist() == (t + k_acc + 1).tolist()
+    new_tails = st.ctx_tail.cpu().numpy()
+    for b in sample:
+        win = np.arange(L[b], L[b] + c.n_nodes)
+        for cache, old in zip((st.k_cache, st.v_cache), before[b]):
+            want, _ = CM.commit_kv(old, 0, int(k_acc[b]), acc["out_nodes"][b])
+            assert np.array_equal(seq_rows(cache, st.block_table[b], win, c.page), want), f"seq {b}"
+        row, _ = CM.commit_tail(tails[b], int(t[b]), acc["out_tokens"][b, :k_acc[b] + 1])
+        assert new_tails[b].tolist() == row.tolist(), f"seq {b}"
+
+
 @pytest.mark.parametrize("name", list(FULL))
 def test_full_size_sampled(name):
     cfg = W.CONFIGS[name]
@@ -113,6 +145,8 @@ def test_full_size_sampled(name):
         assert_accept_equal(acc, b, want[b], cfg.max_depth)
     say(f"full-size {name}: insertion")
     st.insert()
+    say(f"full-size {name}: commit")
+    check_commit(st, acc, sample)
     if cfg.runahead_streams:
         ids = st.caches.new_streams(B)
         st.caches.insert(tw.seq_prompt, ids, tw.runahead)
