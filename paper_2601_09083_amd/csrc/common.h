@@ -54,7 +54,8 @@ struct alignas(256) WsHeader {
 };
 
 // Stream record: [0] prompt (-1 = unbound), [1] tokens appended so far,
-// [2 .. 2+D-2] the last min(len, D-1) tokens, oldest first.
+// [2 + j - 1] the node of the stream's suffix of length j, j = 1 ..
+// min(appended, D-1) (its active nodes; kNone if the table was full).
 constexpr int kStreamHead = 2;
 
 struct TrieView {

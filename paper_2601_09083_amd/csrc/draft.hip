@@ -38,16 +38,19 @@ struct DraftArgs {
 
 struct Smem {
   double sel_score[kMaxN];
-  uint32_t sel_slot[kMaxN];
+  uint32_t sel_first[kMaxN];  // head of the node's child list
   int32_t sel_tok[kMaxN];
   int16_t sel_par[kMaxN];
   uint16_t sel_rank[kMaxN];
   uint8_t sel_depth[kMaxN];
   double f_score[kFrontier];
-  uint32_t f_slot[kFrontier];
+  uint32_t f_first[kFrontier];
   int32_t f_tok[kFrontier];
   uint16_t f_par[kFrontier];
-  uint32_t child[kChildBuf];
+  // one list segment: count, token and child-list head of each child
+  uint32_t c_count[kChildBuf];
+  int32_t c_tok[kChildBuf];
+  uint32_t c_first[kChildBuf];
   uint32_t cursor;
   int nbuf;
 };
@@ -101,14 +104,22 @@ __device__ inline Key frontier_key(const Smem& sm, int e) {
   return make_key(sm.f_score[e], sm.sel_depth[par] + 1, sm.sel_rank[par], sm.f_tok[e], e);
 }
 
-// Lane 0 gathers up to kChildBuf list entries starting at sm.cursor.
+// Lane 0 walks up to kChildBuf list entries starting at sm.cursor.  For
+// each child the next pointer, count, token and the child's own list head
+// are loaded together, so a list of k children costs k dependent loads and
+// nothing more (a selected node's list head was fetched when it became a
+// candidate).
 __device__ inline int gather_children(const TrieView& t, Smem& sm, int lane) {
   if (lane == 0) {
     uint32_t c = sm.cursor;
     int k = 0;
     while (c != kNone && k < kChildBuf) {
-      sm.child[k++] = c;
-      c = t.next[c];
+      const uint32_t nx = t.next[c];
+      sm.c_count[k] = t.count[c];
+      sm.c_tok[k] = static_cast<int32_t>(t.keys[c] & 0xFFFFFFFFull);
+      sm.c_first[k] = t.first[c];
+      ++k;
+      c = nx;
     }
     sm.cursor = c;
     sm.nbuf = k;
@@ -119,25 +130,26 @@ __device__ inline int gather_children(const TrieView& t, Smem& sm, int lane) {
 
 // Pushes the children of selected node `i` onto the frontier.
 __device__ void expand(const TrieView& t, Smem& sm, int i, int lane, int& fsize) {
-  const uint32_t slot = sm.sel_slot[i];
   const double ps = sm.sel_score[i];
   const int cdepth = sm.sel_depth[i] + 1;
   const int prank = sm.sel_rank[i];
 
-  // Pass 1: the sum of the children's counts (the denominator of C).
-  if (lane == 0) sm.cursor = t.first[slot];
+  // Pass 1: the sum of the children's counts (the denominator of C); a list
+  // that fits one segment stays in LDS for pass 2.
+  if (lane == 0) sm.cursor = sm.sel_first[i];
   __syncthreads();
   uint64_t total = 0;
   int segments = 0, k;
   do {
     k = gather_children(t, sm, lane);
-    const uint64_t c = lane < k ? t.count[sm.child[lane]] : 0u;
+    const uint64_t c = lane < k ? sm.c_count[lane] : 0u;
     total += wave_sum_u64(c);
     ++segments;
-    __syncthreads();
+    if (sm.cursor != kNone) __syncthreads();
   } while (sm.cursor != kNone);
   if (segments > 1) {  // long list: walk it again
-    if (lane == 0) sm.cursor = t.first[slot];
+    __syncthreads();
+    if (lane == 0) sm.cursor = sm.sel_first[i];
     __syncthreads();
   }
   const double dtotal = static_cast<double>(total);
@@ -149,16 +161,16 @@ __device__ void expand(const TrieView& t, Smem& sm, int i, int lane, int& fsize)
     int32_t tok = 0;
     uint32_t cs = kNone;
     if (lane < k) {
-      cs = sm.child[lane];
-      const double cv = static_cast<double>(t.count[cs]) / dtotal;  // C(v)
-      sc = ps * cv;                                                   // path product
-      tok = static_cast<int32_t>(t.keys[cs] & 0xFFFFFFFFull);
+      cs = sm.c_first[lane];
+      const double cv = static_cast<double>(sm.c_count[lane]) / dtotal;  // C(v)
+      sc = ps * cv;                                                       // path product
+      tok = sm.c_tok[lane];
     }
     if (fsize + k <= kFrontier) {
       if (lane < k) {
         const int e = fsize + lane;
         sm.f_score[e] = sc;
-        sm.f_slot[e] = cs;
+        sm.f_first[e] = cs;
         sm.f_tok[e] = tok;
         sm.f_par[e] = static_cast<uint16_t>(i);
       }
@@ -172,7 +184,7 @@ __device__ void expand(const TrieView& t, Smem& sm, int i, int lane, int& fsize)
         if (fsize < kFrontier) {
           if (lane == 0) {
             sm.f_score[fsize] = jsc;
-            sm.f_slot[fsize] = jslot;
+            sm.f_first[fsize] = jslot;
             sm.f_tok[fsize] = jtok;
             sm.f_par[fsize] = static_cast<uint16_t>(i);
           }
@@ -192,7 +204,7 @@ __device__ void expand(const TrieView& t, Smem& sm, int i, int lane, int& fsize)
         if (replace && lane == 0) {
           const int e = static_cast<int>(worst.lo & 0x7FF);
           sm.f_score[e] = jsc;
-          sm.f_slot[e] = jslot;
+          sm.f_first[e] = jslot;
           sm.f_tok[e] = jtok;
           sm.f_par[e] = static_cast<uint16_t>(i);
         }
@@ -224,19 +236,18 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
   // Longest suffix with a continuation: lane q-1 tries length q.
   const int qlim = pvalid ? min(min(tlen, Q), D - 1) : 0;
   const int q = lane + 1;
-  uint32_t node = kNone;
-  bool valid = false;
+  uint32_t node = kNone, head = kNone;
   if (q <= qlim) {
     node = t.roots[p];
     for (int i = 0; i < q && node != kNone; ++i) {
       const int32_t x = tail[Q - q + i];
       node = x < 0 ? kNone : trie_lookup(t, node, static_cast<uint32_t>(x));
     }
-    valid = node != kNone && t.first[node] != kNone;
+    if (node != kNone) head = t.first[node];
   }
-  const uint64_t ballot = __ballot(valid);
+  const uint64_t ballot = __ballot(head != kNone);
   const int qstar = ballot ? 64 - __clzll(static_cast<long long>(ballot)) : 0;
-  const uint32_t u = __shfl(node, qstar > 0 ? qstar - 1 : 0, SRT_WAVE);
+  const uint32_t u_head = __shfl(head, qstar > 0 ? qstar - 1 : 0, SRT_WAVE);  // child list of u
 
   int budget = N - 1;
   if (a.alpha > 0.0 && qstar > 0) {
@@ -246,7 +257,7 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
   const int limit = qstar > 0 ? min(a.Dmax, D - qstar) : 0;
 
   if (lane == 0) {
-    sm.sel_slot[0] = u;
+    sm.sel_first[0] = qstar > 0 ? u_head : kNone;
     sm.sel_tok[0] = root_tok;
     sm.sel_par[0] = -1;
     sm.sel_depth[0] = 0;
@@ -266,7 +277,7 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
     best = wave_max(best);
     const int e = static_cast<int>(best.lo & 0x7FF);
     const double sc = sm.f_score[e];
-    const uint32_t cs = sm.f_slot[e];
+    const uint32_t cs = sm.f_first[e];
     const int32_t tok = sm.f_tok[e];
     const int par = sm.f_par[e];
     const int depth = sm.sel_depth[par] + 1;
@@ -274,7 +285,7 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
     __syncthreads();
     if (lane == 0 && e != fsize - 1) {  // remove entry e
       sm.f_score[e] = sm.f_score[fsize - 1];
-      sm.f_slot[e] = sm.f_slot[fsize - 1];
+      sm.f_first[e] = sm.f_first[fsize - 1];
       sm.f_tok[e] = sm.f_tok[fsize - 1];
       sm.f_par[e] = sm.f_par[fsize - 1];
     }
@@ -291,7 +302,7 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
     }
     before = wave_sum_i(before);
     if (lane == 0) {
-      sm.sel_slot[nsel] = cs;
+      sm.sel_first[nsel] = cs;
       sm.sel_tok[nsel] = tok;
       sm.sel_par[nsel] = static_cast<int16_t>(par);
       sm.sel_depth[nsel] = static_cast<uint8_t>(depth);

@@ -9,13 +9,17 @@
 //
 // GPU design: one workgroup per inserted segment; its threads walk
 // independent chains, one per start position k of a substring that ends in
-// the new segment (k may lie up to D-1 tokens before the segment, in the
-// stream's remembered tail).  Chain k descends from the prompt's root along
-// tokens k, k+1, ... creating nodes on demand (hash CAS) and adding one to
-// the count of each node whose substring ends in the new segment.  Chains
-// are independent, so a segment of n tokens exposes n + D - 1 parallel
-// walks of depth <= D; count updates commute, so the resulting map does not
-// depend on scheduling.
+// the new segment.  A stream remembers its active nodes -- the nodes of its
+// suffixes of length 1 .. D-1 -- so a chain that starts j tokens before the
+// segment starts at the active node of length j instead of walking from the
+// root; a chain that starts inside the segment starts at the prompt's root.
+// Chain k descends along the segment's tokens creating nodes on demand (hash
+// CAS) and adds one to the count of each node it reaches (every such
+// substring ends in the new segment).  A segment of n tokens exposes
+// n + D - 1 parallel chains of at most min(n, D) steps, so appending a few
+// tokens costs a few dependent probes; count updates commute, so the
+// resulting map does not depend on scheduling.  The chains that reach the
+// end of the segment with fewer than D tokens are the new active nodes.
 #include <algorithm>
 #include <cstring>
 
@@ -46,7 +50,7 @@ bool make_layout(const srt_trie_config& c, Layout* L) {
     if (slots > (uint64_t(1) << kMaxSlotsLog2)) return false;
   }
   L->slots = slots;
-  L->stream_stride = kStreamHead + c.max_depth;
+  L->stream_stride = kStreamHead + c.max_depth;  // active nodes of lengths 1..D-1 (+1 spare)
   uint64_t off = align256(sizeof(WsHeader));
   L->off_roots = off;
   off = align256(off + sizeof(uint32_t) * static_cast<uint64_t>(c.n_prompts));
@@ -97,7 +101,8 @@ __global__ __launch_bounds__(256) void insert_kernel(void* ws, const int32_t* __
   const int D = t.depth;
   const int entry = blockIdx.x;
   __shared__ int s_ok, s_m;
-  __shared__ int32_t s_prev[64];
+  __shared__ uint32_t s_act[64];
+  __shared__ uint32_t s_created;
   __shared__ int32_t* s_rec;
 
   const int p = prompt_ids[entry];
@@ -130,6 +135,7 @@ __global__ __launch_bounds__(256) void insert_kernel(void* ws, const int32_t* __
     s_ok = ok;
     s_m = m;
     s_rec = rec;
+    s_created = 0;
   }
   __syncthreads();
   if (!s_ok) return;
@@ -142,33 +148,64 @@ __global__ __launch_bounds__(256) void insert_kernel(void* ws, const int32_t* __
     return;
   }
 
+  // Active nodes before the segment: s_act[j-1] = node of the suffix of
+  // length j (j = 1..m).
   const int m = s_m;
   int32_t* rec = s_rec;
-  if (threadIdx.x < m) s_prev[threadIdx.x] = rec[kStreamHead + (D - 1 - m) + threadIdx.x];
+  if (threadIdx.x < m) s_act[threadIdx.x] = static_cast<uint32_t>(rec[kStreamHead + threadIdx.x]);
   __syncthreads();
 
   const uint32_t root = t.roots[p];
   const int chains = m + len;
   for (int c = threadIdx.x; c < chains; c += blockDim.x) {
     const int k = c - m;  // start of the substring, relative to the segment
-    uint32_t node = root;
-    int depth = 0;
-    for (int j = k; j < 0 && node != kNone; ++j, ++depth) node = trie_get_or_create(t, node, s_prev[m + j]);
-    for (int j = k < 0 ? 0 : k; j < len && depth < D && node != kNone; ++j, ++depth) {
-      node = trie_get_or_create(t, node, static_cast<uint32_t>(tok[j]));
-      if (node != kNone) atomicAdd(&t.count[node], 1u);
+    uint32_t node = k < 0 ? s_act[-k - 1] : root;
+    int depth = k < 0 ? -k : 0;
+    int j = k < 0 ? 0 : k;
+    // Each step is one round trip: the probe is the CAS itself (a failed
+    // CAS returns the slot's key), and the child-list push of a node created
+    // in the previous step is issued together with this step's probe.
+    uint32_t link = kNone, link_parent = 0;
+    for (; j < len && depth < D && node != kNone; ++j, ++depth) {
+      const uint64_t key = node_key(node, static_cast<uint32_t>(tok[j]));
+      uint64_t h = mix64(key) & t.mask;
+      uint32_t prev = kNone;
+      if (link != kNone) prev = atomicExch(&t.first[link_parent], link);
+      unsigned long long old = atomicCAS(&t.keys[h], kEmptyKey, (unsigned long long)key);
+      if (link != kNone) t.next[link] = prev;
+      uint64_t probes = 1;
+      while (old != kEmptyKey && old != key && probes <= t.mask) {
+        h = (h + 1) & t.mask;
+        old = atomicCAS(&t.keys[h], kEmptyKey, (unsigned long long)key);
+        ++probes;
+      }
+      if (old != kEmptyKey && old != key) {  // every slot taken
+        set_flag(t, SRT_FLAG_CAPACITY);
+        node = kNone;
+        link = kNone;
+        break;
+      }
+      if (old == kEmptyKey) {
+        link = static_cast<uint32_t>(h);
+        link_parent = node;
+        atomicAdd(&s_created, 1u);
+      } else {
+        link = kNone;
+      }
+      node = static_cast<uint32_t>(h);
+      atomicAdd(&t.count[node], 1u);
     }
+    if (link != kNone) t.next[link] = atomicExch(&t.first[link_parent], link);
+    // A chain that consumed the whole segment with fewer than D tokens ends
+    // at the new active node of its length.
+    if (j == len && depth < D && depth >= 1) rec[kStreamHead + depth - 1] = static_cast<int32_t>(node);
   }
   __syncthreads();
-
   if (threadIdx.x == 0) {
-    // Remember the last min(total, D-1) tokens, right-aligned, oldest first.
-    const int keep = min(m + len, D - 1);
-    for (int r = 0; r < keep; ++r) {
-      const int src = m + len - keep + r;  // index into prev ++ tok
-      rec[kStreamHead + (D - 1 - keep) + r] = src < m ? s_prev[src] : tok[src - m];
-    }
     rec[1] = rec[1] + len;
+    // Nodes created by this segment are counted against the capacity once.
+    const unsigned long long n = atomicAdd(&t.hdr->used, static_cast<unsigned long long>(s_created));
+    if (n + s_created > t.hdr->node_limit) set_flag(t, SRT_FLAG_CAPACITY);
   }
 }
 
