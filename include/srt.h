@@ -200,11 +200,20 @@ int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d, int3
  * of tokens the sequence appends (ready as `lengths` for srt_trie_insert
  * with tokens = out_tokens, stride Dmax+1).  Inputs must be finite (results
  * are unspecified otherwise).
+ * scratch: device buffer, 256-byte aligned, of at least
+ * srt_accept_scratch_bytes(B) bytes (else SRT_ERR_CAPACITY): per-sequence
+ * step barriers of the workgroups that share one walk.  Owned by the
+ * caller; contents are overwritten; calls sharing a scratch buffer must not
+ * overlap.  (A walk whose workgroups could not all meet -- impossible when
+ * the launch succeeds -- reports n_accepted[b] = -1.)
  * ---------------------------------------------------------------------- */
+size_t srt_accept_scratch_bytes(int32_t B);
+
 int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits,
                const float* gumbel, float inv_temperature, const int32_t* tree_tokens,
                const int32_t* tree_parent, const int32_t* n_nodes, int32_t* n_accepted,
-               int32_t* out_tokens, int32_t* out_nodes, int32_t* n_emitted, void* stream);
+               int32_t* out_tokens, int32_t* out_nodes, int32_t* n_emitted, void* scratch,
+               size_t scratch_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Commit of the accepted path (Section 3: the verification pass keeps the

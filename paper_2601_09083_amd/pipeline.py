@@ -119,6 +119,7 @@ class VerifyState:
     logits: Optional[torch.Tensor] = None
     gumbel: Optional[torch.Tensor] = None
     acc: dict = field(default_factory=dict)
+    accept_scratch: Optional[torch.Tensor] = None
     extra_streams: int = 0
 
     # ---- set-up ---------------------------------------------------------
@@ -180,9 +181,12 @@ class VerifyState:
                                  scratch=self.scratch)
 
     def accept(self, inv_temperature: float = 1.0):
+        if self.accept_scratch is None:
+            self.accept_scratch = torch.empty(max(srt.srt_accept_scratch_bytes(self.tokens.batch), 1),
+                                              dtype=torch.uint8, device=self.device)
         self.acc = srt.srt_accept(self.logits, self.gumbel, inv_temperature, self.tree["tree_tokens"],
                                   self.tree["tree_parent"], self.tree["n_nodes"], self.cfg.max_depth,
-                                  out=self.acc or None)
+                                  out=self.acc or None, scratch=self.accept_scratch)
         return self.acc
 
     def insert(self):

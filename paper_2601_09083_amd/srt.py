@@ -25,7 +25,7 @@ _NAMES = {SRT_ERR_INVALID: "SRT_ERR_INVALID", SRT_ERR_CAPACITY: "SRT_ERR_CAPACIT
 # Every symbol include/srt.h declares.
 EXPORTS = ("srt_trie_workspace_bytes", "srt_trie_init", "srt_trie_insert", "srt_trie_reset_streams",
            "srt_trie_status", "srt_trie_export", "srt_draft", "srt_tree_attn_scratch_bytes",
-           "srt_tree_attn", "srt_accept", "srt_commit", "srt_version")
+           "srt_tree_attn", "srt_accept_scratch_bytes", "srt_accept", "srt_commit", "srt_version")
 
 
 class SrtError(RuntimeError):
@@ -67,7 +67,8 @@ def lib() -> ctypes.CDLL:
             "srt_draft": (ctypes.c_int, [_P, _I32, _P, _P, _P, ctypes.POINTER(DraftParams), _P, _P, _P, _P, _P, _P]),
             "srt_tree_attn_scratch_bytes": (_SZ, [_I32] * 7),
             "srt_tree_attn": (ctypes.c_int, [_I32] * 7 + [_I64] + [_P] * 7 + [ctypes.c_float, _P, _P, _SZ, _P]),
-            "srt_accept": (ctypes.c_int, [_I32] * 4 + [_P, _P, ctypes.c_float] + [_P] * 8),
+            "srt_accept_scratch_bytes": (_SZ, [_I32]),
+            "srt_accept": (ctypes.c_int, [_I32] * 4 + [_P, _P, ctypes.c_float] + [_P] * 7 + [_P, _SZ, _P]),
             "srt_commit": (ctypes.c_int, [_I32] * 6 + [_I64] + [_P] * 4 + [_I32] + [_P] * 3 + [_I32, _P, _P, _P]),
             "srt_version": (ctypes.c_char_p, []),
         }
@@ -206,8 +207,12 @@ def srt_tree_attn(q, k_cache, v_cache, block_table, ctx_len, tree_parent, n_node
 
 # --------------------------------------------------------------------------- acceptance
 
+def srt_accept_scratch_bytes(B: int) -> int:
+    return int(lib().srt_accept_scratch_bytes(B))
+
+
 def srt_accept(logits, gumbel, inv_temperature: float, tree_tokens, tree_parent, n_nodes, max_depth: int,
-               out=None, stream=None) -> dict:
+               out=None, scratch=None, stream=None) -> dict:
     """logits [B,N,V] fp32; gumbel [B,max_depth+1,V] fp32 or None (greedy)."""
     B, N, V = logits.shape
     if gumbel is not None and tuple(gumbel.shape) != (B, max_depth + 1, V):
@@ -218,12 +223,16 @@ def srt_accept(logits, gumbel, inv_temperature: float, tree_tokens, tree_parent,
                "out_tokens": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
                "out_nodes": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
                "n_emitted": torch.empty(B, dtype=torch.int32, device=dev)}
+    need = srt_accept_scratch_bytes(B)
+    if scratch is None or scratch.numel() < need:
+        scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     _check("srt_accept", lib().srt_accept(
         B, N, V, max_depth, _ptr(logits, torch.float32, "logits"), _ptr(gumbel, torch.float32, "gumbel"),
         float(inv_temperature), _ptr(tree_tokens, torch.int32, "tree_tokens"),
         _ptr(tree_parent, torch.int32, "tree_parent"), _ptr(n_nodes, torch.int32, "n_nodes"),
         _ptr(out["n_accepted"], torch.int32), _ptr(out["out_tokens"], torch.int32),
-        _ptr(out["out_nodes"], torch.int32), _ptr(out.get("n_emitted"), torch.int32), _stream(stream)))
+        _ptr(out["out_nodes"], torch.int32), _ptr(out.get("n_emitted"), torch.int32), _ptr(scratch, name="scratch"),
+        scratch.numel(), _stream(stream)))
     return out
 
 

@@ -81,11 +81,24 @@ def test_host_validation_before_any_hip_call():
     assert L.srt_tree_attn(*args) == S.SRT_ERR_INVALID               # N > 256
     args[1] = 8; args[6] = 2052
     assert L.srt_tree_attn(*args) == S.SRT_ERR_CAPACITY              # scratch needed, none given
-    acc = [4, 0, 16, 4, None, None, 1.0] + [None] * 7 + [None]
+    acc = [4, 0, 16, 4, None, None, 1.0] + [None] * 7 + [None, 0, None]
     assert L.srt_accept(*acc) == S.SRT_ERR_INVALID                   # N = 0
     acc[1] = 8; acc[3] = 64
     assert L.srt_accept(*acc) == S.SRT_ERR_INVALID                   # Dmax > 63
     acc[3] = 4
     assert L.srt_accept(*acc) == S.SRT_ERR_INVALID                   # null pointers
+    acc[4:14] = [ctypes.c_void_p(256)] * 2 + [1.0] + [ctypes.c_void_p(256)] * 7
+    assert L.srt_accept(*acc) == S.SRT_ERR_CAPACITY                  # scratch needed, none given
+    acc[14], acc[15] = ctypes.c_void_p(256 + 16), S.srt_accept_scratch_bytes(4)
+    assert L.srt_accept(*acc) == S.SRT_ERR_INVALID                   # scratch not 256-byte aligned
     acc[0] = 0
     assert L.srt_accept(*acc) == S.SRT_OK                            # B = 0
+    assert S.srt_accept_scratch_bytes(4) >= 4 * 256 and S.srt_accept_scratch_bytes(-1) == 0
+    com = [4, 8, 1, 64, 16, 40, 100] + [None] * 4 + [4] + [None] * 3 + [8, None, None, None]
+    assert L.srt_commit(*com) == S.SRT_ERR_INVALID                   # null pointers
+    com[3] = 12
+    assert L.srt_commit(*com) == S.SRT_ERR_UNSUPPORTED               # d not a multiple of 8
+    com[3] = 64; com[16] = ctypes.c_void_p(256)
+    assert L.srt_commit(*com) == S.SRT_ERR_INVALID                   # ctx_tail without draft_len
+    com[0] = 0; com[16] = None
+    assert L.srt_commit(*com) == S.SRT_OK                            # B = 0
