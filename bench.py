@@ -71,6 +71,57 @@ def counter_traffic():
         return None
 
 
+ATTN_KERNELS = ("tree_attn_plan_kernel", "tree_attn_kernel<128>", "tree_attn_combine_kernel<128>")
+
+
+def _short_name(name):
+    n = name.replace("(anonymous namespace)::", "").replace("void ", "")
+    return n.split("(")[0]
+
+
+def write_counter_file(d):
+    """HBM traffic per srt_tree_attn launch from four rocprofv3 --pmc runs in
+    directory d: pmc_FETCH_SIZE / pmc_WRITE_SIZE of `bench.py --no-cpu-baseline
+    --steps 5 --warmup 1` and pmc_copy_* of `bench.py --copy-calibration`.
+    Each counter is scaled by what it reads for a 1 GiB device copy.  Only
+    the launches of the timed steps are used; their algorithmic bytes come
+    from the bench line the same run printed."""
+    import csv
+
+    def per_dispatch(sub):
+        out = {}
+        for r in csv.DictReader(open(os.path.join(d, sub, "run_counter_collection.csv"))):
+            out.setdefault(_short_name(r["Kernel_Name"]), []).append(
+                (int(r["Dispatch_Id"]), float(r["Counter_Value"])))
+        return {k: [v for _, v in sorted(x)] for k, x in out.items()}
+
+    res = {"source_sha256": source_sha(ATTN_SRC),
+           "kernel": "srt_tree_attn = " + " + ".join(ATTN_KERNELS) + " (Qwen2.5-7B-shaped workload)",
+           "calibration": {}, "per_kernel_bytes": {}}
+    per_launch = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        cp = per_dispatch(f"pmc_copy_{c}").get("__amd_rocclr_copyBuffer", [])
+        big = sorted(cp)[-5:]  # the five 1 GiB copies
+        kib = float(np.median(big))
+        factor = (1 << 30) / 1024.0 / kib
+        res["calibration"][c] = {"copy_kib_per_GiB": kib, "factor": factor}
+        run = per_dispatch(f"pmc_{c}")
+        for k in ATTN_KERNELS:
+            vals = run.get(k, [])[-5:]  # launches of the 5 timed steps
+            b = float(np.mean(vals)) * 1024.0 * factor if vals else 0.0
+            res["per_kernel_bytes"][k] = res["per_kernel_bytes"].get(k, 0.0) + b
+            per_launch[c] = per_launch.get(c, 0.0) + b
+    res["fetch_bytes_per_launch"] = per_launch["FETCH_SIZE"]
+    res["write_bytes_per_launch"] = per_launch["WRITE_SIZE"]
+    res["hbm_bytes_per_launch"] = per_launch["FETCH_SIZE"] + per_launch["WRITE_SIZE"]
+    line = [l for l in open(os.path.join(d, "pmc_FETCH_SIZE.log")) if l.startswith("{")][-1]
+    alg = json.loads(line)["roofline"]["algorithmic_bytes"]
+    res["algorithmic_bytes_per_launch"] = alg
+    res["traffic_over_algorithmic"] = res["hbm_bytes_per_launch"] / alg
+    json.dump(res, open(COUNTERS, "w"), indent=1)
+    print(json.dumps(res, indent=1))
+
+
 def cpu_baseline(st, tree_np, budget_s: float):
     """The oracle, as it stands, on a bounded sample of the same workload:
     per sequence the draft (from the prompt's stream index), fp64 tree
@@ -135,7 +186,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
+    ap.add_argument("--counters-from", metavar="DIR",
+                    help="write the attention HBM-traffic file from rocprofv3 --pmc runs in DIR and exit")
     args = ap.parse_args()
+    if args.counters_from:
+        write_counter_file(args.counters_from)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
               f"(the path shards per prompt, see the design notes)", file=sys.stderr)
