@@ -25,6 +25,15 @@ Readings (the paper leaves these open):
 * the tree is emitted in selection order: node 0 is the last committed token
   (parent -1, depth 0), then the selected nodes, each with the index of its
   parent in this list and its depth relative to u_q.
+
+Drafting variants (Section 3 leaves the form of the budget B(q) open; the
+example of Fig. 2 drafts the single highest-scoring path):
+* score threshold: with min_score > 0 only candidates whose path-product
+  score is >= min_score are drafted (still at most B of them); since the
+  order is score-descending these are a prefix of it;
+* chain: with chain=True every node contributes only its best child (largest
+  C(v), i.e. largest count, then smallest token id), so the candidates, and
+  the draft, form one path.
 """
 from __future__ import annotations
 
@@ -42,10 +51,10 @@ def longest_match(trie, tail: Sequence[int], t: int, qmax: int) -> int:
     return best
 
 
-def candidates(trie, s: Tuple[int, ...], depth_limit: int):
-    """Every descendant of node s within ``depth_limit`` edges, with its fp64
-    path-product score: list of (score, path) where path is the token tuple
-    from s."""
+def candidates(trie, s: Tuple[int, ...], depth_limit: int, chain: bool = False):
+    """Every descendant of node s within ``depth_limit`` edges (only the best
+    child of each node when ``chain``), with its fp64 path-product score:
+    list of (score, path) where path is the token tuple from s."""
     out = []
 
     def visit(node: Tuple[int, ...], path: Tuple[int, ...], score: float):
@@ -53,8 +62,11 @@ def candidates(trie, s: Tuple[int, ...], depth_limit: int):
             return
         kids = trie.children(node)
         total = float(sum(kids.values()))
-        for x, c in kids.items():
-            cv = float(c) / total           # C(v), one fp64 division
+        items = list(kids.items())
+        if chain and items:
+            items = [min(items, key=lambda xc: (-xc[1], xc[0]))]  # largest count, then smallest token
+        for x, c in items:
+            cv = float(c) / total           # C(v), one fp64 division (denominator over all children)
             sv = score * cv                 # path product, one fp64 multiplication
             out.append((sv, path + (x,)))
             visit(node + (x,), path + (x,), sv)
@@ -64,7 +76,7 @@ def candidates(trie, s: Tuple[int, ...], depth_limit: int):
 
 
 def draft(trie, tail: Sequence[int], t: int, qmax: int, n_nodes: int, max_depth: int,
-          budget_alpha: float = 0.0):
+          budget_alpha: float = 0.0, min_score: float = 0.0, chain: bool = False):
     """Draft tree for one sequence.
 
     ``tail`` holds the last min(t, Qmax) committed tokens (right-aligned; any
@@ -78,8 +90,10 @@ def draft(trie, tail: Sequence[int], t: int, qmax: int, n_nodes: int, max_depth:
         return tokens, parents, depths, 1, 0
     s = tuple(tail[len(tail) - q:])
     limit = min(max_depth, trie.D - q)
-    cands = candidates(trie, s, limit)
+    cands = candidates(trie, s, limit, chain)
     cands.sort(key=lambda c: (-c[0], len(c[1]), c[1]))
+    if min_score > 0:
+        cands = [c for c in cands if c[0] >= min_score]
     budget = n_nodes - 1
     if budget_alpha > 0:
         budget = min(budget, int(math.floor(budget_alpha * q)))
@@ -93,7 +107,8 @@ def draft(trie, tail: Sequence[int], t: int, qmax: int, n_nodes: int, max_depth:
     return tokens, parents, depths, len(tokens), q
 
 
-def draft_batch(tries: List, prompt_ids, tails, ts, qmax, n_nodes, max_depth, budget_alpha=0.0):
+def draft_batch(tries: List, prompt_ids, tails, ts, qmax, n_nodes, max_depth, budget_alpha=0.0, min_score=0.0,
+                chain=False):
     """``draft`` for every sequence; outputs padded to N with -1 like the GPU."""
     import numpy as np
     B = len(ts)
@@ -104,7 +119,7 @@ def draft_batch(tries: List, prompt_ids, tails, ts, qmax, n_nodes, max_depth, bu
     ml = np.zeros(B, dtype=np.int32)
     for b in range(B):
         tok, par, dep, n, q = draft(tries[int(prompt_ids[b])], tails[b], int(ts[b]), qmax,
-                                    n_nodes, max_depth, budget_alpha)
+                                    n_nodes, max_depth, budget_alpha, min_score, chain)
         tt[b, :n], tp[b, :n], td[b, :n] = tok, par, dep
         nn[b], ml[b] = n, q
     return tt, tp, td, nn, ml

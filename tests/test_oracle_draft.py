@@ -39,10 +39,12 @@ def test_golden(golden_dir):
                                          c["match_len"]), c
 
 
-def best_first(trie, tail, t, qmax, N, Dmax, alpha=0.0):
+def best_first(trie, tail, t, qmax, N, Dmax, alpha=0.0, min_score=0.0, chain=False):
     """Greedy expansion with a priority queue: pop the best frontier node, add
-    its children; the match scans q downward and stops at the first suffix
-    that has a continuation."""
+    its children (only the one with the largest count, then smallest token,
+    for chain drafts) and stop at the budget or, with a threshold, at the
+    first popped score below it; the match scans q downward and stops at the
+    first suffix that has a continuation."""
     tail = list(tail)
     root = tail[-1] if t >= 1 else -1
     q = 0
@@ -63,7 +65,8 @@ def best_first(trie, tail, t, qmax, N, Dmax, alpha=0.0):
             return
         kids = trie.children(s + node_path)
         tot = float(sum(kids.values()))
-        for x, c in kids.items():
+        items = sorted(kids.items(), key=lambda xc: (-xc[1], xc[0]))
+        for x, c in (items[:1] if chain else items):
             sc = score * (float(c) / tot)
             heapq.heappush(heap, (-sc, len(node_path) + 1, node_path + (x,), idx))
 
@@ -71,6 +74,8 @@ def best_first(trie, tail, t, qmax, N, Dmax, alpha=0.0):
     push((), 0, 1.0)
     while heap and len(tok) - 1 < budget:
         negs, d, path, pidx = heapq.heappop(heap)
+        if min_score > 0 and -negs < min_score:
+            break
         tok.append(path[-1]); par.append(pidx); dep.append(d)
         push(path, len(tok) - 1, -negs)
     return tok, par, dep, len(tok), q
@@ -94,6 +99,72 @@ def test_best_first_equals_sort_all(seed):
     rng = random.Random(seed)
     trie, tail, t, qmax, N, Dmax = rand_case(rng)
     assert DR.draft(trie, tail, t, qmax, N, Dmax) == best_first(trie, tail, t, qmax, N, Dmax)
+
+
+@pytest.mark.parametrize("seed", range(200))
+def test_best_first_equals_sort_all_variants(seed):
+    rng = random.Random(5000 + seed)
+    trie, tail, t, qmax, N, Dmax = rand_case(rng)
+    chain = seed % 2 == 1
+    tau = [0.0, 0.05, 0.2, 1.0 / 3.0, 0.5][seed % 5]
+    assert DR.draft(trie, tail, t, qmax, N, Dmax, min_score=tau, chain=chain) == \
+        best_first(trie, tail, t, qmax, N, Dmax, min_score=tau, chain=chain)
+
+
+def chain_walk(trie, tail, t, qmax, N, Dmax, min_score=0.0):
+    """Chain draft by hand: from the match, repeatedly take the child with the
+    largest count (smallest token on ties) while the running product of
+    C = count / sum of sibling counts stays >= min_score."""
+    q = DR.longest_match(trie, tail, t, qmax)
+    tok = [tail[-1] if t >= 1 else -1]
+    if q == 0:
+        return tok, q
+    node = tuple(tail[-q:])
+    score = 1.0
+    for _ in range(min(N - 1, min(Dmax, trie.D - q))):
+        kids = trie.children(node)
+        if not kids:
+            break
+        x = max(kids, key=lambda k: (kids[k], -k))
+        score = score * (kids[x] / sum(kids.values()))
+        if min_score > 0 and score < min_score:
+            break
+        tok.append(x)
+        node = node + (x,)
+    return tok, q
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_chain_equals_walk(seed):
+    rng = random.Random(9000 + seed)
+    trie, tail, t, qmax, N, Dmax = rand_case(rng)
+    tau = [0.0, 0.1, 0.4][seed % 3]
+    tok, par, dep, n, q = DR.draft(trie, tail, t, qmax, N, Dmax, min_score=tau, chain=True)
+    assert (tok, q) == chain_walk(trie, tail, t, qmax, N, Dmax, tau)
+    assert par == list(range(-1, n - 1)) and dep == list(range(n))
+
+
+def test_chain_hand_case():
+    # after "1": 2 follows three times, 7 once; after "1 2": 3 twice, 6 once
+    streams = [[1, 2, 3, 4, 5], [1, 2, 3, 4, 5], [1, 2, 6], [1, 7]]
+    trie = T.DictTrie(T.substring_counts(streams, 8), 8)
+    tok, par, dep, n, q = DR.draft(trie, [1], 1, 1, 10, 6, chain=True)
+    assert q == 1 and tok == [1, 2, 3, 4, 5] and par == [-1, 0, 1, 2, 3]
+    tok, *_ = DR.draft(trie, [1], 1, 1, 10, 6, min_score=0.5, chain=True)
+    assert tok == [1, 2, 3, 4, 5]          # 3/4, then 3/4 * 2/3 = 1/2 exactly, kept (>=)
+    tok, *_ = DR.draft(trie, [1], 1, 1, 10, 6, min_score=0.5 + 1e-12, chain=True)
+    assert tok == [1, 2]
+
+
+def test_threshold_is_a_prefix_of_the_order():
+    streams = [[1, 2, 3, 4, 5], [1, 2, 3, 4, 5], [1, 6, 7], [1, 6, 8], [1, 6, 9], [1, 6, 10]]
+    trie = T.DictTrie(T.substring_counts(streams, 8), 8)
+    full = DR.draft(trie, [1], 1, 1, 7, 5)
+    assert full[0] == [1, 6, 2, 3, 4, 5, 7]  # scores 2/3, 1/3, 1/3, 1/3, 1/3, 1/6
+    tok, *_ = DR.draft(trie, [1], 1, 1, 7, 5, min_score=1.0 / 3.0)
+    assert tok == [1, 6, 2, 3, 4, 5]
+    tok, *_ = DR.draft(trie, [1], 1, 1, 7, 5, min_score=0.5)
+    assert tok == [1, 6]
 
 
 @pytest.mark.parametrize("seed", range(100))
@@ -201,6 +272,48 @@ def _no_child_requirement(trie, tail, t, qmax, N, Dmax, alpha=0.0):
     tok, par, dep, n, q = DR.draft(Wrapped(), tail, t, qmax, N, Dmax, alpha)
     keep = [i for i in range(n) if tok[i] != -5 or i == 0]
     return [tok[i] for i in keep], [par[i] for i in keep], [dep[i] for i in keep], len(keep), q
+
+
+def _strict_threshold(trie, tail, t, qmax, N, Dmax, min_score=0.0, chain=False):
+    tok, par, dep, n, q = DR.draft(trie, tail, t, qmax, N, Dmax, chain=chain)
+    s = tuple(tail[-q:]) if q else ()
+    keep = 1
+    scores = {(): 1.0}
+    paths = {0: ()}
+    for i in range(1, n):
+        paths[i] = paths[par[i]] + (tok[i],)
+        kids = trie.children(s + paths[par[i]])
+        sc = scores[paths[par[i]]] * (kids[tok[i]] / sum(kids.values()))
+        scores[paths[i]] = sc
+        if min_score > 0 and not sc > min_score:
+            break
+        keep += 1
+    return tok[:keep], par[:keep], dep[:keep], keep, q
+
+
+def _chain_by_token(trie, tail, t, qmax, N, Dmax, min_score=0.0):
+    q = DR.longest_match(trie, tail, t, qmax)
+    tok = [tail[-1] if t >= 1 else -1]
+    if q == 0:
+        return tok, q
+    node = tuple(tail[-q:])
+    for _ in range(min(N - 1, min(Dmax, trie.D - q))):
+        kids = trie.children(node)
+        if not kids:
+            break
+        x = min(kids)  # smallest token instead of largest count
+        tok.append(x)
+        node = node + (x,)
+    return tok, q
+
+
+def test_variant_pins_catch_planted_mistakes():
+    streams = [[1, 2, 3, 4, 5], [1, 2, 3, 4, 5], [1, 2, 6], [1, 7]]
+    trie = T.DictTrie(T.substring_counts(streams, 8), 8)
+    assert _strict_threshold(trie, [1], 1, 1, 10, 6, 0.5, True)[0] != [1, 2, 3, 4, 5]
+    streams = [[1, 9, 3], [1, 9, 3], [1, 2, 3]]
+    trie = T.DictTrie(T.substring_counts(streams, 8), 8)
+    assert _chain_by_token(trie, [1], 1, 1, 10, 6)[0] != DR.draft(trie, [1], 1, 1, 10, 6, chain=True)[0]
 
 
 def test_pins_catch_planted_mistakes(golden_dir):
