@@ -125,7 +125,9 @@ int srt_trie_export(const void* ws, int32_t prompt_id, int64_t max_nodes, int32_
  *   score(u) = 1.  They are ranked by score (descending), then relative
  *   depth (ascending), then token path from u (lexicographic by token id),
  *   and the first B are drafted, B = max_nodes - 1, or
- *   min(max_nodes - 1, floor(budget_alpha * q*)) when budget_alpha > 0.
+ *   min(max_nodes - 1, floor(budget_alpha * q*)) when budget_alpha > 0;
+ *   with min_score > 0 only those of score >= min_score; chain drafts keep
+ *   only each node's best child among the candidates.
  * Output tree (row-major [B, max_nodes] int32, rows >= n_nodes[b] set to -1):
  *   node 0 = last committed token (ctx_tail[b, max_match-1], -1 if t == 0),
  *   parent -1, depth 0; nodes 1.. = drafted nodes in rank order, each with
@@ -137,8 +139,12 @@ typedef struct {
   int32_t max_match;     /* Qmax: 1..64, columns of ctx_tail */
   int32_t max_nodes;     /* N: tree rows including the root, 1..256 */
   int32_t max_depth;     /* Dmax: 0..63 */
-  int32_t reserved;      /* must be 0 */
+  int32_t chain;         /* 0: tree draft; 1: chain draft -- every node
+                            contributes only its best child (largest count,
+                            then smallest token), so the draft is one path */
   double budget_alpha;   /* <= 0: budget N-1 */
+  double min_score;      /* <= 0: off; else only candidates whose score is
+                            >= min_score are drafted (at most B of them) */
 } srt_draft_params;
 
 int srt_draft(const void* ws, int32_t B, const int32_t* prompt_ids, const int32_t* ctx_tail,

@@ -7,6 +7,11 @@
 // counts of v's siblings (the displayed equation of Section 3) and drafted
 // greedily up to the budget.
 //
+// Drafting variants: with min_score > 0 selection stops at the first
+// candidate whose path-product score is below it (candidates leave the
+// frontier in score order), and chain drafts push only the best child of
+// each selected node, found while the child list is summed.
+//
 // GPU design: one wavefront per sequence.  Lane q-1 walks the suffix of
 // length q from the root (all q in parallel) and a ballot picks the longest
 // one that has a child.  Expansion keeps the candidate frontier in LDS; each
@@ -32,8 +37,8 @@ constexpr int kFrontier = 512;  // frontier capacity, >= 2 * kMaxN
 constexpr int kChildBuf = 64;   // children gathered per list segment
 
 struct DraftArgs {
-  int32_t Q, N, Dmax;
-  double alpha;
+  int32_t Q, N, Dmax, chain;
+  double alpha, min_score;
 };
 
 struct Smem {
@@ -128,8 +133,9 @@ __device__ inline int gather_children(const TrieView& t, Smem& sm, int lane) {
   return sm.nbuf;
 }
 
-// Pushes the children of selected node `i` onto the frontier.
-__device__ void expand(const TrieView& t, Smem& sm, int i, int lane, int& fsize) {
+// Pushes the children of selected node `i` onto the frontier (only the best
+// one -- largest count, then smallest token -- for chain drafts).
+__device__ void expand(const TrieView& t, Smem& sm, int i, int lane, int& fsize, bool chain) {
   const double ps = sm.sel_score[i];
   const int cdepth = sm.sel_depth[i] + 1;
   const int prank = sm.sel_rank[i];
@@ -140,13 +146,44 @@ __device__ void expand(const TrieView& t, Smem& sm, int i, int lane, int& fsize)
   __syncthreads();
   uint64_t total = 0;
   int segments = 0, k;
+  // best child so far: key (count << 32 | 0x7FFFFFFF - token), its list head
+  uint64_t best_key = 0;
+  uint32_t best_first = kNone;
   do {
     k = gather_children(t, sm, lane);
     const uint64_t c = lane < k ? sm.c_count[lane] : 0u;
     total += wave_sum_u64(c);
+    if (chain) {
+      const uint64_t key = lane < k ? (c << 32) | static_cast<uint32_t>(0x7FFFFFFF - sm.c_tok[lane]) : 0ull;
+      uint64_t mx = key;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        const uint64_t o = shfl_xor_u64(mx, off);
+        mx = o > mx ? o : mx;
+      }
+      const uint64_t hit = __ballot(lane < k && key == mx);  // sibling tokens are distinct
+      if (mx > best_key) {
+        best_key = mx;
+        best_first = __shfl(lane < k ? sm.c_first[lane] : kNone, __ffsll(static_cast<long long>(hit)) - 1, SRT_WAVE);
+      }
+    }
     ++segments;
     if (sm.cursor != kNone) __syncthreads();
   } while (sm.cursor != kNone);
+  if (chain) {
+    if (best_key != 0 && fsize < kFrontier) {
+      if (lane == 0) {
+        const double cv = static_cast<double>(static_cast<uint32_t>(best_key >> 32)) / static_cast<double>(total);
+        sm.f_score[fsize] = ps * cv;  // C(v), then the path product
+        sm.f_first[fsize] = best_first;
+        sm.f_tok[fsize] = static_cast<int32_t>(0x7FFFFFFF - static_cast<uint32_t>(best_key & 0xFFFFFFFFull));
+        sm.f_par[fsize] = static_cast<uint16_t>(i);
+      }
+      ++fsize;
+    }
+    __syncthreads();
+    return;
+  }
   if (segments > 1) {  // long list: walk it again
     __syncthreads();
     if (lane == 0) sm.cursor = sm.sel_first[i];
@@ -266,7 +303,8 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
   }
   __syncthreads();
   int nsel = 1, fsize = 0;
-  if (qstar > 0 && budget > 0 && limit > 0) expand(t, sm, 0, lane, fsize);
+  const bool chain = a.chain != 0;
+  if (qstar > 0 && budget > 0 && limit > 0) expand(t, sm, 0, lane, fsize, chain);
 
   while (nsel - 1 < budget && fsize > 0) {
     Key best{0ull, 0ull};
@@ -277,6 +315,7 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
     best = wave_max(best);
     const int e = static_cast<int>(best.lo & 0x7FF);
     const double sc = sm.f_score[e];
+    if (a.min_score > 0.0 && sc < a.min_score) break;  // every remaining candidate scores lower
     const uint32_t cs = sm.f_first[e];
     const int32_t tok = sm.f_tok[e];
     const int par = sm.f_par[e];
@@ -311,7 +350,7 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
     }
     __syncthreads();
     ++nsel;
-    if (depth < limit) expand(t, sm, nsel - 1, lane, fsize);
+    if (depth < limit) expand(t, sm, nsel - 1, lane, fsize, chain);
   }
 
   const int64_t row = static_cast<int64_t>(b) * N;
@@ -336,13 +375,14 @@ extern "C" int srt_draft(const void* ws, int32_t B, const int32_t* prompt_ids, c
   if (!ws || !params || B < 0) return SRT_ERR_INVALID;
   const srt_draft_params& p = *params;
   if (p.max_match < 1 || p.max_match > 64 || p.max_nodes < 1 || p.max_nodes > kMaxN || p.max_depth < 0 ||
-      p.max_depth > 63 || p.reserved != 0 || !(p.budget_alpha == p.budget_alpha))
+      p.max_depth > 63 || (p.chain != 0 && p.chain != 1) || !(p.budget_alpha == p.budget_alpha) ||
+      !(p.min_score == p.min_score))
     return SRT_ERR_INVALID;
   if (B == 0) return SRT_OK;
   if (!prompt_ids || !ctx_tail || !ctx_len || !tree_tokens || !tree_parent || !tree_depth || !n_nodes ||
       !match_len)
     return SRT_ERR_INVALID;
-  DraftArgs a{p.max_match, p.max_nodes, p.max_depth, p.budget_alpha};
+  DraftArgs a{p.max_match, p.max_nodes, p.max_depth, p.chain, p.budget_alpha, p.min_score};
   draft_kernel<<<B, 64, 0, as_stream(stream)>>>(ws, prompt_ids, ctx_tail, ctx_len, a, tree_tokens, tree_parent,
                                                tree_depth, n_nodes, match_len);
   return launch_status();

@@ -169,10 +169,11 @@ class VerifyState:
         self.gumbel = W.make_gumbel(self.cfg, self.tokens.batch, device=self.device) if sampled else None
 
     # ---- the four calls of one step ---------------------------------------
-    def draft(self, alpha: float = 0.0):
+    def draft(self, alpha: float = 0.0, min_score: float = 0.0, chain: bool = False):
         c = self.cfg
         self.tree = srt.srt_draft(self.caches.ws, self.prompt_ids, self.ctx_tail, self.draft_len, c.max_match,
-                                  c.n_nodes, c.max_depth, alpha, out=self.tree or None)
+                                  c.n_nodes, c.max_depth, alpha, out=self.tree or None, min_score=min_score,
+                                  chain=chain)
         return self.tree
 
     def attention(self):

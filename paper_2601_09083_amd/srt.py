@@ -42,8 +42,8 @@ class TrieConfig(ctypes.Structure):
 
 class DraftParams(ctypes.Structure):
     _fields_ = [("max_match", ctypes.c_int32), ("max_nodes", ctypes.c_int32),
-                ("max_depth", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("budget_alpha", ctypes.c_double)]
+                ("max_depth", ctypes.c_int32), ("chain", ctypes.c_int32),
+                ("budget_alpha", ctypes.c_double), ("min_score", ctypes.c_double)]
 
 
 _lib = None
@@ -157,7 +157,7 @@ def srt_trie_export(ws: torch.Tensor, prompt_id: int, max_nodes: int, stream=Non
 # --------------------------------------------------------------------------- draft
 
 def srt_draft(ws: torch.Tensor, prompt_ids, ctx_tail, ctx_len, max_match: int, max_nodes: int, max_depth: int,
-              budget_alpha: float = 0.0, out=None, stream=None) -> dict:
+              budget_alpha: float = 0.0, out=None, stream=None, min_score: float = 0.0, chain: bool = False) -> dict:
     B = int(prompt_ids.numel())
     if ctx_tail.shape != (B, max_match):
         raise ValueError("ctx_tail must be [B, max_match]")
@@ -167,7 +167,7 @@ def srt_draft(ws: torch.Tensor, prompt_ids, ctx_tail, ctx_len, max_match: int, m
                for k in ("tree_tokens", "tree_parent", "tree_depth")}
         out["n_nodes"] = torch.empty(B, dtype=torch.int32, device=dev)
         out["match_len"] = torch.empty(B, dtype=torch.int32, device=dev)
-    prm = DraftParams(max_match, max_nodes, max_depth, 0, float(budget_alpha))
+    prm = DraftParams(max_match, max_nodes, max_depth, int(bool(chain)), float(budget_alpha), float(min_score))
     _check("srt_draft", lib().srt_draft(
         _ptr(ws, torch.uint8, "ws"), B, _ptr(prompt_ids, torch.int32, "prompt_ids"),
         _ptr(ctx_tail, torch.int32, "ctx_tail"), _ptr(ctx_len, torch.int32, "ctx_len"), ctypes.byref(prm),

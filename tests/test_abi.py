@@ -70,6 +70,10 @@ def test_host_validation_before_any_hip_call():
     assert L.srt_draft(ctypes.c_void_p(256), 1, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
     p = S.DraftParams(8, 8, 64, 0, 0.0)    # Dmax > 63
     assert L.srt_draft(ctypes.c_void_p(256), 1, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
+    p = S.DraftParams(8, 8, 4, 2, 0.0)    # chain must be 0 or 1
+    assert L.srt_draft(ctypes.c_void_p(256), 1, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
+    p = S.DraftParams(8, 8, 4, 0, 0.0, float("nan"))  # min_score NaN
+    assert L.srt_draft(ctypes.c_void_p(256), 1, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
     p = S.DraftParams(8, 8, 4, 0, 0.0)
     assert L.srt_draft(ctypes.c_void_p(256), 0, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_OK  # B = 0
     assert L.srt_draft(ctypes.c_void_p(256), 2, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID

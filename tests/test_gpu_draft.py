@@ -1,6 +1,7 @@
 """GPU parity of srt_draft against the oracle draft, bit-exact: the tiny
 configuration, random small-vocabulary caches full of score ties, budget and
-depth variants, fallbacks, and a frontier overflow."""
+depth variants, score thresholds and chain drafts, fallbacks, and a frontier
+overflow (also with chain drafts over a 1500-child list)."""
 import random
 
 import numpy as np
@@ -17,10 +18,10 @@ from tests.gpu_util import assert_tree_equal, oracle_draft_rows, oracle_trie, sa
 pytestmark = pytest.mark.gpu
 
 
-def run_draft(c, prompt_ids, tails, ts, Q, N, Dmax, alpha=0.0):
+def run_draft(c, prompt_ids, tails, ts, Q, N, Dmax, alpha=0.0, min_score=0.0, chain=False):
     dev = "cuda"
     t = lambda a: torch.as_tensor(np.asarray(a, dtype=np.int32), device=dev)
-    out = srt.srt_draft(c.ws, t(prompt_ids), t(tails), t(ts), Q, N, Dmax, alpha)
+    out = srt.srt_draft(c.ws, t(prompt_ids), t(tails), t(ts), Q, N, Dmax, alpha, min_score=min_score, chain=chain)
     return tree_to_np(out)
 
 
@@ -49,14 +50,18 @@ def test_random_small_vocab_ties(seed):
     c.insert([p for p in range(P) for _ in streams[p]], ids, [x for s in streams for x in s])
     tries = [TR.DictTrie(TR.substring_counts(streams[p], D), D) for p in range(P)]
     Q = rng.randrange(1, min(D, 9))
-    for N, Dmax, alpha in [(rng.randrange(1, 40), rng.randrange(0, 10), 0.0), (256, 63, 0.0), (64, 12, 1.7)]:
-        say(f"draft: seed={seed} D={D} vocab={vocab} Q={Q} N={N} Dmax={Dmax} alpha={alpha}")
+    variants = [(rng.randrange(1, 40), rng.randrange(0, 10), 0.0, 0.0, False), (256, 63, 0.0, 0.0, False),
+                (64, 12, 1.7, 0.0, False), (64, 12, 0.0, 0.1, False), (256, 63, 0.0, 1.0 / 3.0, False),
+                (64, 12, 0.0, 0.0, True), (64, 12, 0.0, 0.05, True), (32, 4, 2.5, 0.0, True)]
+    for N, Dmax, alpha, tau, chain in variants:
+        say(f"draft: seed={seed} D={D} vocab={vocab} Q={Q} N={N} Dmax={Dmax} alpha={alpha} tau={tau} chain={chain}")
         pids = [rng.randrange(P) for _ in range(B)]
         tails = [[rng.randrange(vocab) for _ in range(Q)] for _ in range(B)]
         ts = [rng.choice([0, 1, 2, Q, 100]) for _ in range(B)]
-        tree = run_draft(c, pids, tails, ts, Q, N, Dmax, alpha)
+        tree = run_draft(c, pids, tails, ts, Q, N, Dmax, alpha, tau, chain)
         for b in range(B):
-            want = DR.draft(tries[pids[b]], tails[b][Q - min(ts[b], Q):] if ts[b] else [], ts[b], Q, N, Dmax, alpha)
+            want = DR.draft(tries[pids[b]], tails[b][Q - min(ts[b], Q):] if ts[b] else [], ts[b], Q, N, Dmax, alpha,
+                            tau, chain)
             assert_tree_equal(tree, b, want)
 
 
@@ -74,6 +79,32 @@ def test_frontier_overflow_and_long_child_lists():
         say(f"draft: frontier overflow N={N} Dmax={Dmax}")
         tree = run_draft(c, [0], [[7]], [5], 1, N, Dmax)
         assert_tree_equal(tree, 0, DR.draft(trie, [7], 5, 1, N, Dmax))
+    for tau, chain in [(0.0, True), (1e-4, False), (1e-3, True)]:
+        say(f"draft: long child list tau={tau} chain={chain}")
+        tree = run_draft(c, [0], [[7]], [5], 1, 256, 2, 0.0, tau, chain)
+        assert_tree_equal(tree, 0, DR.draft(trie, [7], 5, 1, 256, 2, 0.0, tau, chain))
+
+
+@pytest.mark.parametrize("tau,chain", [(0.0, True), (0.02, False)])
+def test_qwen1p5b_variants_full_batch(tau, chain):
+    cfg = W.CONFIGS["qwen1.5b"]
+    say(f"draft: qwen1.5b tau={tau} chain={chain}")
+    st = VerifyState.build(cfg)
+    tree = tree_to_np(st.draft(min_score=tau, chain=chain))
+    tw = st.tokens
+    rng = np.random.default_rng(11)
+    sample = sorted(set(int(x) for x in rng.choice(tw.batch, 6, replace=False)))
+    tails, ts = tw.ctx_tail(), tw.draft_len()
+    for b in sample:
+        p = int(tw.seq_prompt[b])
+        trie = oracle_trie(tw.streams_of_prompt(p), cfg.trie_depth, big=True)
+        want = DR.draft(trie, tails[b], int(ts[b]), cfg.max_match, cfg.n_nodes, cfg.max_depth, 0.0, tau, chain)
+        assert_tree_equal(tree, b, want)
+    if chain:
+        n = tree["n_nodes"]
+        par = tree["tree_parent"]
+        for b in range(tw.batch):
+            assert (par[b, 1:n[b]] == np.arange(n[b] - 1)).all()
 
 
 def test_deterministic_across_runs():
