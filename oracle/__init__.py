@@ -25,8 +25,13 @@ method computes, written from the paper (SRT, arXiv 2601.09083):
 * ``commit``    -- the accepted path's key/value vectors moved into the
                    committed positions and the context advanced (Section 3,
                    classic speculative decoding; Appendix C).
+* ``lmhead``    -- the acceptance walk with the policy's logits at each
+                   visited node formed by its LM head on that node's hidden
+                   state (Section 3's single verification pass), in fp64
+                   rounded once to fp32, with the bound for other fp32
+                   summation orders.
 
 Pins (tests marked ``not gpu``) tie each function to closed forms, brute
 force, library routines and invariants; see ``tests/test_oracle_*.py``.
 """
-from . import accept, attention, commit, draft, trie  # noqa: F401
+from . import accept, attention, commit, draft, lmhead, trie  # noqa: F401
