@@ -175,6 +175,82 @@ def cpu_baseline(st, tree_np, budget_s: float):
                       f"(draft + fp64 tree attention + acceptance + insert + commit), {t_total:.1f} s on 1 thread"}
 
 
+def fused_head(st, cfg, calls: int, unfused: bool):
+    """The acceptance walk with the LM head fused in (srt_accept_lmhead) on
+    the current trees: synthetic bf16 head [V, d_model] and hidden states
+    [B, N, d_model] (d_model = Hq * head_dim, the model width of the
+    Qwen2.5 shapes), a node's hidden state planted with its first child's
+    head row at the workload's boost rate; the same Gumbel noise.  Timed
+    with events around each call; the roofline counts, per level that had
+    walking sequences, the head once plus the walkers' hidden rows and noise
+    rows.  With ``unfused`` the LM head over every node (hipBLASLt bf16 GEMM
+    to fp32 logits) followed by srt_accept is timed too, for comparison."""
+    import torch
+
+    from paper_2601_09083_amd import srt
+    from paper_2601_09083_amd import workload as W
+
+    B, N, V, dm = st.tokens.batch, cfg.n_nodes, cfg.vocab, cfg.hq * cfg.head_dim
+    tree = {k: v.cpu().numpy() for k, v in st.tree.items()}
+    hidden, w = W.make_head(B, N, dm, V, device="cuda", seed=4242, kind="normal", tree_tokens=tree["tree_tokens"],
+                            tree_parent=tree["tree_parent"], n_nodes=tree["n_nodes"], plant_p=cfg.boost_p)
+    scratch = torch.empty(srt.srt_accept_lmhead_scratch_bytes(B, V), dtype=torch.uint8, device="cuda")
+    args = (hidden, w, st.gumbel, 1.0, st.tree["tree_tokens"], st.tree["tree_parent"], st.tree["n_nodes"],
+            cfg.max_depth)
+    out = srt.srt_accept_lmhead(*args, scratch=scratch)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
+    stream = torch.cuda.current_stream()
+    for e0, e1 in ev:
+        e0.record(stream)
+        srt.srt_accept_lmhead(*args, out=out, scratch=scratch)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    emitted = out["n_emitted"].cpu().numpy().astype(np.int64)
+    levels = int(emitted.max())
+    walkers = [int((emitted > l).sum()) for l in range(levels)]  # sequences walking at level l
+    per_level_head = V * dm * 2
+    nbytes = sum(per_level_head + n * (dm * 2 + (V * 4 if st.gumbel is not None else 0)) for n in walkers)
+    flops = sum(2.0 * n * dm * V for n in walkers)
+    res = {"ms": ms, "d_model": dm, "levels": levels, "walkers_per_level": walkers,
+           "mean_emitted": float(emitted.mean()),
+           "roofline": {"bound": "hbm", "achieved": nbytes / (ms / 1e3) / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                        "frac": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, "algorithmic_bytes": float(nbytes),
+                        "algorithmic_flops": flops, "mfma_tflops": flops / (ms / 1e3) / 1e12}}
+    if unfused:
+        # the unfused path: LM head over all B*N nodes, then the logits walk
+        x = hidden.reshape(B * N, dm)
+        wt = w.t().contiguous()
+        logits = torch.empty((B, N, V), dtype=torch.float32, device="cuda")
+        acc = None
+        t = []
+        kind = "torch.mm bf16 -> fp32 logits over all B*N nodes + srt_accept"
+        try:
+            torch.mm(x[:64], wt, out_dtype=torch.float32, out=logits.view(B * N, V)[:64])
+            head = lambda: torch.mm(x, wt, out_dtype=torch.float32, out=logits.view(B * N, V))
+        except (NotImplementedError, RuntimeError, TypeError):
+            kind = "torch.mm bf16 logits over all B*N nodes, converted to fp32, + srt_accept"
+            head = lambda: logits.view(B * N, V).copy_(torch.mm(x, wt))
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            head()
+            acc = srt.srt_accept(logits, st.gumbel, 1.0, st.tree["tree_tokens"], st.tree["tree_parent"],
+                                 st.tree["n_nodes"], cfg.max_depth, out=acc, scratch=st.accept_scratch)
+            e1.record(stream)
+            t.append((e0, e1))
+        torch.cuda.synchronize()
+        res["unfused_ms"] = float(np.mean([a.elapsed_time(b) for a, b in t[1:]]))
+        res["unfused_kind"] = kind
+        same = bool(torch.equal(acc["n_accepted"], out["n_accepted"]))
+        res["unfused_same_n_accepted"] = same
+        del logits, wt
+    del hidden, w, scratch
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -184,6 +260,9 @@ def main():
     ap.add_argument("--greedy", action="store_true", help="greedy acceptance instead of T=1 sampling")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--head-calls", type=int, default=10,
+                    help="timed calls of the fused LM-head walk (0: skip it)")
+    ap.add_argument("--no-unfused", action="store_true", help="skip timing the unfused LM head + walk")
     ap.add_argument("--part-steps", type=int, default=20,
                     help="steps of the separate pass that times every part with its own events")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -330,6 +409,8 @@ def main():
         "mean_emitted": n_emit / args.steps / B,
         "roofline": roof,
     }
+    if args.head_calls > 0:
+        res["fused_head"] = fused_head(st, cfg, args.head_calls, not args.no_unfused)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(st, tree_np, args.cpu_budget)
     print(json.dumps(res), flush=True)

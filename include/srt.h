@@ -9,6 +9,8 @@
  *   srt_tree_attn  -> attention of every tree node over context + ancestors
  *   (caller)       -> LM head: per-node logits
  *   srt_accept     -> accepted path + bonus token
+ *   (or srt_accept_lmhead: the LM head and the walk fused, on the visited
+ *    nodes only)
  *   srt_trie_insert-> emitted tokens appended to the sequence's stream
  *   srt_commit     -> accepted nodes' K/V moved into place, context advanced
  *
@@ -220,6 +222,45 @@ int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logit
                const int32_t* tree_parent, const int32_t* n_nodes, int32_t* n_accepted,
                int32_t* out_tokens, int32_t* out_nodes, int32_t* n_emitted, void* scratch,
                size_t scratch_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Acceptance walk with the LM head applied at the visited nodes only
+ * (Sections 1 and 3: the single verification pass supplies the policy's
+ * next-token distribution at every drafted node; the walk needs it only at
+ * the nodes it visits).
+ *
+ * Same walk, outputs and conventions as srt_accept, with
+ *   logits[b,u,j] = sum_k hidden[b,u,k] * w_head[j,k]
+ * formed on demand for the visited nodes (fp32 sums of the exact bf16
+ * products; the summation order is the kernel's, so a logit may differ from
+ * the correctly rounded dot product by the fp32 rounding of its additions,
+ * and with it an arg-max whose top two scores are that close; with inputs
+ * whose partial sums are exact in fp32 the result equals srt_accept on the
+ * materialised logits bit for bit).  No [B, N, V] logits tensor is formed.
+ * The walk advances one depth level per kernel pair for the whole batch
+ * (Dmax + 1 pairs are always enqueued; a level with no walking sequence
+ * exits at once); each level reads the head once.
+ * Layouts: hidden [B, N, d_model] bf16 bits (the final hidden state of each
+ * tree node), w_head [V, d_model] bf16 bits, both 16-byte aligned; gumbel
+ * [B, Dmax+1, V] fp32 or NULL (greedy; inv_temperature then unused, else it
+ * must be finite); tree arrays and outputs as srt_accept (unused entries
+ * of out_tokens / out_nodes are -1).  d_model must be a multiple of 64
+ * (else SRT_ERR_UNSUPPORTED); 0 <= Dmax <= 63.
+ * scratch: device buffer, 256-byte aligned, of at least
+ * srt_accept_lmhead_scratch_bytes(B, V) bytes (else SRT_ERR_CAPACITY):
+ * per-level lists of walking sequences and their per-tile arg-max
+ * candidates (8 bytes per sequence per 128 vocabulary entries).  Owned by
+ * the caller; contents are overwritten; calls sharing a scratch buffer must
+ * not overlap.
+ * ---------------------------------------------------------------------- */
+size_t srt_accept_lmhead_scratch_bytes(int32_t B, int32_t V);
+
+int srt_accept_lmhead(int32_t B, int32_t N, int32_t d_model, int32_t V, int32_t Dmax,
+                      const uint16_t* hidden, const uint16_t* w_head, const float* gumbel,
+                      float inv_temperature, const int32_t* tree_tokens, const int32_t* tree_parent,
+                      const int32_t* n_nodes, int32_t* n_accepted, int32_t* out_tokens,
+                      int32_t* out_nodes, int32_t* n_emitted, void* scratch, size_t scratch_bytes,
+                      void* stream);
 
 /* ------------------------------------------------------------------------
  * Commit of the accepted path (Section 3: the verification pass keeps the

@@ -34,17 +34,20 @@ from . import accept as _accept
 U32 = 2.0 ** -24  # unit roundoff of fp32
 
 
-def head_logits(hidden_row, w_head) -> np.ndarray:
-    """fp32 logits of one node: fp64 dot products rounded once to fp32.
+def head_logits(hidden_rows, w_head) -> np.ndarray:
+    """fp32 logits: fp64 dot products rounded once to fp32.
 
-    hidden_row [d] and w_head [V, d] hold bf16-representable values."""
-    h = np.asarray(hidden_row, dtype=np.float64)
+    hidden_rows [d] (one node -> [V]) or [n, d] (n nodes -> [n, V]) and
+    w_head [V, d] hold bf16-representable values."""
+    h = np.asarray(hidden_rows, dtype=np.float64)
+    h2 = h[None, :] if h.ndim == 1 else h
     W = np.asarray(w_head)
-    out = np.empty(W.shape[0], dtype=np.float64)
-    step = 8192  # rows per block, only to bound the fp64 temporary
+    out = np.empty((W.shape[0], h2.shape[0]), dtype=np.float64)
+    step = 8192  # head rows per block, only to bound the fp64 temporary
     for j0 in range(0, W.shape[0], step):
-        out[j0:j0 + step] = W[j0:j0 + step].astype(np.float64) @ h
-    return out.astype(np.float32)
+        out[j0:j0 + step] = W[j0:j0 + step].astype(np.float64) @ h2.T
+    out = out.T.astype(np.float32)
+    return out[0] if h.ndim == 1 else out
 
 
 def logit_error_bound(hidden_row, w_head) -> np.ndarray:

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libsrt.so")
-SOURCES = ["trie.hip", "draft.hip", "tree_attn.hip", "accept.hip", "commit.hip"]
+SOURCES = ["trie.hip", "draft.hip", "tree_attn.hip", "accept.hip", "lmhead.hip", "commit.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -25,7 +25,8 @@ _NAMES = {SRT_ERR_INVALID: "SRT_ERR_INVALID", SRT_ERR_CAPACITY: "SRT_ERR_CAPACIT
 # Every symbol include/srt.h declares.
 EXPORTS = ("srt_trie_workspace_bytes", "srt_trie_init", "srt_trie_insert", "srt_trie_reset_streams",
            "srt_trie_status", "srt_trie_export", "srt_draft", "srt_tree_attn_scratch_bytes",
-           "srt_tree_attn", "srt_accept_scratch_bytes", "srt_accept", "srt_commit", "srt_version")
+           "srt_tree_attn", "srt_accept_scratch_bytes", "srt_accept", "srt_accept_lmhead_scratch_bytes",
+           "srt_accept_lmhead", "srt_commit", "srt_version")
 
 
 class SrtError(RuntimeError):
@@ -69,6 +70,8 @@ def lib() -> ctypes.CDLL:
             "srt_tree_attn": (ctypes.c_int, [_I32] * 7 + [_I64] + [_P] * 7 + [ctypes.c_float, _P, _P, _SZ, _P]),
             "srt_accept_scratch_bytes": (_SZ, [_I32]),
             "srt_accept": (ctypes.c_int, [_I32] * 4 + [_P, _P, ctypes.c_float] + [_P] * 7 + [_P, _SZ, _P]),
+            "srt_accept_lmhead_scratch_bytes": (_SZ, [_I32, _I32]),
+            "srt_accept_lmhead": (ctypes.c_int, [_I32] * 5 + [_P, _P, _P, ctypes.c_float] + [_P] * 7 + [_P, _SZ, _P]),
             "srt_commit": (ctypes.c_int, [_I32] * 6 + [_I64] + [_P] * 4 + [_I32] + [_P] * 3 + [_I32, _P, _P, _P]),
             "srt_version": (ctypes.c_char_p, []),
         }
@@ -233,6 +236,42 @@ def srt_accept(logits, gumbel, inv_temperature: float, tree_tokens, tree_parent,
         _ptr(out["n_accepted"], torch.int32), _ptr(out["out_tokens"], torch.int32),
         _ptr(out["out_nodes"], torch.int32), _ptr(out.get("n_emitted"), torch.int32), _ptr(scratch, name="scratch"),
         scratch.numel(), _stream(stream)))
+    return out
+
+
+def srt_accept_lmhead_scratch_bytes(B: int, V: int) -> int:
+    return int(lib().srt_accept_lmhead_scratch_bytes(B, V))
+
+
+def srt_accept_lmhead(hidden, w_head, gumbel, inv_temperature: float, tree_tokens, tree_parent, n_nodes,
+                      max_depth: int, out=None, scratch=None, stream=None) -> dict:
+    """hidden [B,N,d_model] bf16; w_head [V,d_model] bf16; gumbel [B,max_depth+1,V]
+    fp32 or None (greedy).  Outputs as srt_accept."""
+    B, N, dm = hidden.shape
+    V, dm2 = w_head.shape
+    if dm2 != dm:
+        raise ValueError("w_head must be [V, d_model]")
+    if gumbel is not None and tuple(gumbel.shape) != (B, max_depth + 1, V):
+        raise ValueError("gumbel must be [B, max_depth+1, V]")
+    if tuple(tree_tokens.shape) != (B, N) or tuple(tree_parent.shape) != (B, N):
+        raise ValueError("tree arrays must be [B, N]")
+    dev = hidden.device
+    if out is None:
+        out = {"n_accepted": torch.empty(B, dtype=torch.int32, device=dev),
+               "out_tokens": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
+               "out_nodes": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
+               "n_emitted": torch.empty(B, dtype=torch.int32, device=dev)}
+    need = srt_accept_lmhead_scratch_bytes(B, V)
+    if scratch is None or scratch.numel() < need:
+        scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check("srt_accept_lmhead", lib().srt_accept_lmhead(
+        B, N, dm, V, max_depth, _ptr(hidden, torch.bfloat16, "hidden"), _ptr(w_head, torch.bfloat16, "w_head"),
+        _ptr(gumbel, torch.float32, "gumbel"), float(inv_temperature),
+        _ptr(tree_tokens, torch.int32, "tree_tokens"), _ptr(tree_parent, torch.int32, "tree_parent"),
+        _ptr(n_nodes, torch.int32, "n_nodes"), _ptr(out["n_accepted"], torch.int32),
+        _ptr(out["out_tokens"], torch.int32), _ptr(out["out_nodes"], torch.int32),
+        _ptr(out.get("n_emitted"), torch.int32), _ptr(scratch, name="scratch"), scratch.numel(),
+        _stream(stream)))
     return out
 
 

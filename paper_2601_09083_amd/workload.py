@@ -355,3 +355,42 @@ def make_gumbel(cfg: Config, batch: int, device="cpu", seed: Optional[int] = Non
     k = torch.randint(1, 1 << 24, shape, generator=g, device=device, dtype=torch.int32)
     u = k.to(torch.float64) * (1.0 / (1 << 24))
     return (-torch.log(-torch.log(u))).to(torch.float32)
+
+
+def make_head(batch: int, n_nodes_max: int, d_model: int, vocab: int, device="cpu", seed: int = 0,
+              kind: str = "normal", tree_tokens: Optional[np.ndarray] = None,
+              tree_parent: Optional[np.ndarray] = None, n_nodes: Optional[np.ndarray] = None,
+              plant_p: float = 0.0, density: float = 1.0):
+    """Final hidden states [B, N, d_model] and LM-head weights [V, d_model],
+    bf16 (synthetic: no trained head).
+
+    kind "normal": N(0, 1) entries rounded to bf16.  kind "int": integers,
+    uniform in [-3, 3] for the head and in [-1, 1] for the hidden states
+    (zero with probability 1 - density), so every dot product and partial
+    sum is an integer far below 2^24.  With probability plant_p a node's
+    hidden state is replaced by the head row of its first drafted child's
+    token (bookkeeping on the given tree, like the logit boost), which makes
+    that token's score large for the walk to follow."""
+    import torch
+    g = _gen(device, seed)
+    if kind == "normal":
+        w = torch.randn((vocab, d_model), generator=g, device=device).to(torch.bfloat16)
+        h = torch.randn((batch, n_nodes_max, d_model), generator=g, device=device).to(torch.bfloat16)
+    elif kind == "int":
+        w = torch.randint(-3, 4, (vocab, d_model), generator=g, device=device).to(torch.bfloat16)
+        h = torch.randint(-1, 2, (batch, n_nodes_max, d_model), generator=g, device=device)
+        if density < 1.0:
+            keep = torch.rand((batch, n_nodes_max, d_model), generator=g, device=device) < density
+            h = h * keep
+        h = h.to(torch.bfloat16)
+    else:
+        raise ValueError(kind)
+    if plant_p > 0.0:
+        bt = boost_tokens(tree_tokens, tree_parent, n_nodes)
+        rng = np.random.Generator(np.random.PCG64(seed + 1))
+        hit = (bt >= 0) & (rng.random(bt.shape) < plant_p)
+        bi, ni = np.nonzero(hit)
+        if bi.size:
+            ti = torch.from_numpy(bt[bi, ni]).to(device)
+            h[torch.from_numpy(bi).to(device), torch.from_numpy(ni).to(device)] = w[ti]
+    return h, w

@@ -98,6 +98,31 @@ def test_host_validation_before_any_hip_call():
     acc[0] = 0
     assert L.srt_accept(*acc) == S.SRT_OK                            # B = 0
     assert S.srt_accept_scratch_bytes(4) >= 4 * 256 and S.srt_accept_scratch_bytes(-1) == 0
+    P = ctypes.c_void_p(256)
+    lmh = [4, 8, 128, 1000, 4, P, P, None, 1.0] + [P] * 6 + [None, P, S.srt_accept_lmhead_scratch_bytes(4, 1000), None]
+    bad = list(lmh); bad[1] = 0
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_INVALID            # N = 0
+    bad = list(lmh); bad[4] = 64
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_INVALID            # Dmax > 63
+    bad = list(lmh); bad[3] = 0
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_INVALID            # V = 0
+    bad = list(lmh); bad[2] = 96
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_UNSUPPORTED        # d_model not a multiple of 64
+    bad = list(lmh); bad[7] = P; bad[8] = float("inf")
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_INVALID            # sampled with a non-finite 1/T
+    bad = list(lmh); bad[6] = ctypes.c_void_p(256 + 8)
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_INVALID            # w_head not 16-byte aligned
+    bad = list(lmh); bad[11] = None
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_INVALID            # null n_nodes
+    bad = list(lmh); bad[16] = ctypes.c_void_p(256 + 64)
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_INVALID            # scratch not 256-byte aligned
+    bad = list(lmh); bad[17] -= 1
+    assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_CAPACITY           # scratch too small
+    bad = list(lmh); bad[0] = 0
+    assert L.srt_accept_lmhead(*bad) == S.SRT_OK                     # B = 0
+    # candidates: 8 bytes per sequence per 128 vocabulary entries, plus lists
+    assert S.srt_accept_lmhead_scratch_bytes(256, 152064) >= 256 * 1188 * 8
+    assert S.srt_accept_lmhead_scratch_bytes(4, 0) == 0 and S.srt_accept_lmhead_scratch_bytes(-1, 10) == 0
     com = [4, 8, 1, 64, 16, 40, 100] + [None] * 4 + [4] + [None] * 3 + [8, None, None, None]
     assert L.srt_commit(*com) == S.SRT_ERR_INVALID                   # null pointers
     com[3] = 12

@@ -164,3 +164,13 @@ def test_batch_clamps_node_counts():
     for b, n in ((0, 1), (1, 5), (2, 5)):
         assert res[b] == LH.accept_lmhead(hidden[b], W, None, 1.0, tt[b], tp[b], n, Dmax)
     assert res[0][0] == 0 and len(res[0][1]) == 1  # a root-only tree emits just the bonus
+
+
+def test_head_logits_rows_match_single():
+    rng = np.random.default_rng(9)
+    W = bf16_round(rng.standard_normal((300, 64)).astype(np.float32))
+    H = bf16_round(rng.standard_normal((5, 64)).astype(np.float32))
+    many = LH.head_logits(H, W)
+    assert many.shape == (5, 300)
+    for i in range(5):
+        assert np.array_equal(many[i], LH.head_logits(H[i], W))
