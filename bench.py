@@ -194,7 +194,7 @@ def fused_head(st, cfg, calls: int, unfused: bool):
     tree = {k: v.cpu().numpy() for k, v in st.tree.items()}
     hidden, w = W.make_head(B, N, dm, V, device="cuda", seed=4242, kind="normal", tree_tokens=tree["tree_tokens"],
                             tree_parent=tree["tree_parent"], n_nodes=tree["n_nodes"], plant_p=cfg.boost_p)
-    scratch = torch.empty(srt.srt_accept_lmhead_scratch_bytes(B, V), dtype=torch.uint8, device="cuda")
+    scratch = torch.empty(srt.srt_accept_lmhead_scratch_bytes(B, N, V), dtype=torch.uint8, device="cuda")
     args = (hidden, w, st.gumbel, 1.0, st.tree["tree_tokens"], st.tree["tree_parent"], st.tree["n_nodes"],
             cfg.max_depth)
     out = srt.srt_accept_lmhead(*args, scratch=scratch)

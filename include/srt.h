@@ -239,7 +239,10 @@ int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logit
  * materialised logits bit for bit).  No [B, N, V] logits tensor is formed.
  * The walk advances one depth level per kernel pair for the whole batch
  * (Dmax + 1 pairs are always enqueued; a level with no walking sequence
- * exits at once); each level reads the head once.
+ * exits at once); each level reads the head once.  Once the subtrees of
+ * the walking sequences' current nodes hold few enough nodes, one pass
+ * computes the arg-max of all of them and every walk is completed from
+ * those (same results: a node's dot product does not depend on the pass).
  * Layouts: hidden [B, N, d_model] bf16 bits (the final hidden state of each
  * tree node), w_head [V, d_model] bf16 bits, both 16-byte aligned; gumbel
  * [B, Dmax+1, V] fp32 or NULL (greedy; inv_temperature then unused, else it
@@ -247,13 +250,15 @@ int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logit
  * of out_tokens / out_nodes are -1).  d_model must be a multiple of 64
  * (else SRT_ERR_UNSUPPORTED); 0 <= Dmax <= 63.
  * scratch: device buffer, 256-byte aligned, of at least
- * srt_accept_lmhead_scratch_bytes(B, V) bytes (else SRT_ERR_CAPACITY):
- * per-level lists of walking sequences and their per-tile arg-max
- * candidates (8 bytes per sequence per 128 vocabulary entries).  Owned by
+ * srt_accept_lmhead_scratch_bytes(B, N, V) bytes (else SRT_ERR_CAPACITY):
+ * per-level lists of walking sequences and of their subtrees' nodes, a
+ * node-to-row table (4 bytes per tree node) and per-tile arg-max
+ * candidates (8 bytes per row per 128 vocabulary entries, for max(B, 128)
+ * rows).  Owned by
  * the caller; contents are overwritten; calls sharing a scratch buffer must
  * not overlap.
  * ---------------------------------------------------------------------- */
-size_t srt_accept_lmhead_scratch_bytes(int32_t B, int32_t V);
+size_t srt_accept_lmhead_scratch_bytes(int32_t B, int32_t N, int32_t V);
 
 int srt_accept_lmhead(int32_t B, int32_t N, int32_t d_model, int32_t V, int32_t Dmax,
                       const uint16_t* hidden, const uint16_t* w_head, const float* gumbel,

@@ -70,7 +70,7 @@ def lib() -> ctypes.CDLL:
             "srt_tree_attn": (ctypes.c_int, [_I32] * 7 + [_I64] + [_P] * 7 + [ctypes.c_float, _P, _P, _SZ, _P]),
             "srt_accept_scratch_bytes": (_SZ, [_I32]),
             "srt_accept": (ctypes.c_int, [_I32] * 4 + [_P, _P, ctypes.c_float] + [_P] * 7 + [_P, _SZ, _P]),
-            "srt_accept_lmhead_scratch_bytes": (_SZ, [_I32, _I32]),
+            "srt_accept_lmhead_scratch_bytes": (_SZ, [_I32, _I32, _I32]),
             "srt_accept_lmhead": (ctypes.c_int, [_I32] * 5 + [_P, _P, _P, ctypes.c_float] + [_P] * 7 + [_P, _SZ, _P]),
             "srt_commit": (ctypes.c_int, [_I32] * 6 + [_I64] + [_P] * 4 + [_I32] + [_P] * 3 + [_I32, _P, _P, _P]),
             "srt_version": (ctypes.c_char_p, []),
@@ -239,8 +239,8 @@ def srt_accept(logits, gumbel, inv_temperature: float, tree_tokens, tree_parent,
     return out
 
 
-def srt_accept_lmhead_scratch_bytes(B: int, V: int) -> int:
-    return int(lib().srt_accept_lmhead_scratch_bytes(B, V))
+def srt_accept_lmhead_scratch_bytes(B: int, N: int, V: int) -> int:
+    return int(lib().srt_accept_lmhead_scratch_bytes(B, N, V))
 
 
 def srt_accept_lmhead(hidden, w_head, gumbel, inv_temperature: float, tree_tokens, tree_parent, n_nodes,
@@ -261,7 +261,7 @@ def srt_accept_lmhead(hidden, w_head, gumbel, inv_temperature: float, tree_token
                "out_tokens": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
                "out_nodes": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
                "n_emitted": torch.empty(B, dtype=torch.int32, device=dev)}
-    need = srt_accept_lmhead_scratch_bytes(B, V)
+    need = srt_accept_lmhead_scratch_bytes(B, N, V)
     if scratch is None or scratch.numel() < need:
         scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     _check("srt_accept_lmhead", lib().srt_accept_lmhead(

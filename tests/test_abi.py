@@ -99,7 +99,7 @@ def test_host_validation_before_any_hip_call():
     assert L.srt_accept(*acc) == S.SRT_OK                            # B = 0
     assert S.srt_accept_scratch_bytes(4) >= 4 * 256 and S.srt_accept_scratch_bytes(-1) == 0
     P = ctypes.c_void_p(256)
-    lmh = [4, 8, 128, 1000, 4, P, P, None, 1.0] + [P] * 6 + [None, P, S.srt_accept_lmhead_scratch_bytes(4, 1000), None]
+    lmh = [4, 8, 128, 1000, 4, P, P, None, 1.0] + [P] * 6 + [None, P, S.srt_accept_lmhead_scratch_bytes(4, 8, 1000), None]
     bad = list(lmh); bad[1] = 0
     assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_INVALID            # N = 0
     bad = list(lmh); bad[4] = 64
@@ -120,9 +120,11 @@ def test_host_validation_before_any_hip_call():
     assert L.srt_accept_lmhead(*bad) == S.SRT_ERR_CAPACITY           # scratch too small
     bad = list(lmh); bad[0] = 0
     assert L.srt_accept_lmhead(*bad) == S.SRT_OK                     # B = 0
-    # candidates: 8 bytes per sequence per 128 vocabulary entries, plus lists
-    assert S.srt_accept_lmhead_scratch_bytes(256, 152064) >= 256 * 1188 * 8
-    assert S.srt_accept_lmhead_scratch_bytes(4, 0) == 0 and S.srt_accept_lmhead_scratch_bytes(-1, 10) == 0
+    # candidates: 8 bytes per row per 128 vocabulary entries, a row table, lists
+    assert S.srt_accept_lmhead_scratch_bytes(256, 64, 152064) >= 256 * 1188 * 8 + 256 * 64 * 4
+    assert S.srt_accept_lmhead_scratch_bytes(4, 8, 1000) >= 128 * 8 * 8  # at least 128 rows
+    assert S.srt_accept_lmhead_scratch_bytes(4, 8, 0) == 0 and S.srt_accept_lmhead_scratch_bytes(-1, 8, 10) == 0
+    assert S.srt_accept_lmhead_scratch_bytes(4, 0, 10) == 0
     com = [4, 8, 1, 64, 16, 40, 100] + [None] * 4 + [4] + [None] * 3 + [8, None, None, None]
     assert L.srt_commit(*com) == S.SRT_ERR_INVALID                   # null pointers
     com[3] = 12

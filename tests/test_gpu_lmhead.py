@@ -135,7 +135,7 @@ def test_depth_cap_root_only_and_clamped_counts():
 
 def test_scratch_reuse_across_sizes():
     rng = random.Random(11)
-    scratch = torch.empty(srt.srt_accept_lmhead_scratch_bytes(300, 3000), dtype=torch.uint8, device="cuda")
+    scratch = torch.empty(srt.srt_accept_lmhead_scratch_bytes(300, 16, 3000), dtype=torch.uint8, device="cuda")
     for B, V, d, seed in ((300, 3000, 128, 1), (17, 700, 64, 2), (300, 3000, 128, 1)):
         N, Dmax = 16, 6
         tree = random_trees(random.Random(seed), B, N, Dmax, V)
