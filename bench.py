@@ -175,15 +175,53 @@ def cpu_baseline(st, tree_np, budget_s: float):
                       f"(draft + fp64 tree attention + acceptance + insert + commit), {t_total:.1f} s on 1 thread"}
 
 
+FINISH_ROWS = 128  # srt_accept_lmhead finishes the walks in one pass at or below this many subtree nodes
+
+
+def head_passes(tree, out_nodes, emitted, Dmax):
+    """Rows of each product pass srt_accept_lmhead made: level l multiplies
+    the current nodes of the sequences still walking, unless the subtrees of
+    those nodes (down to depth Dmax) hold at most FINISH_ROWS nodes, in which
+    case that one pass covers them all and the walks end there.  Rebuilt
+    from the trees and the returned walks (host bookkeeping)."""
+    tp, nn = tree["tree_parent"], tree["n_nodes"]
+    B, N = tp.shape
+    depth = np.full((B, N), -1, dtype=np.int64)
+    depth[:, 0] = 0
+    for c in range(1, N):
+        p = tp[:, c]
+        ok = (p >= 0) & (p < c) & (c < nn)
+        depth[ok, c] = depth[ok, p[ok]] + 1
+
+    def subtree(b, u):
+        n, cnt = int(nn[b]), 0
+        for c in range(u, n):
+            x = c
+            while x > u:
+                x = int(tp[b, x])
+            cnt += int(x == u and 0 <= depth[b, c] <= Dmax)
+        return cnt
+
+    passes = []
+    for l in range(int(emitted.max())):
+        seqs = np.nonzero(emitted > l)[0]
+        cur = [0 if l == 0 else int(out_nodes[b, l - 1]) for b in seqs]
+        total = sum(subtree(int(b), u) for b, u in zip(seqs, cur))
+        if total <= FINISH_ROWS:
+            passes.append(total)
+            break
+        passes.append(len(seqs))
+    return passes
+
+
 def fused_head(st, cfg, calls: int, unfused: bool):
     """The acceptance walk with the LM head fused in (srt_accept_lmhead) on
     the current trees: synthetic bf16 head [V, d_model] and hidden states
     [B, N, d_model] (d_model = Hq * head_dim, the model width of the
     Qwen2.5 shapes), a node's hidden state planted with its first child's
     head row at the workload's boost rate; the same Gumbel noise.  Timed
-    with events around each call; the roofline counts, per level that had
-    walking sequences, the head once plus the walkers' hidden rows and noise
-    rows.  With ``unfused`` the LM head over every node (hipBLASLt bf16 GEMM
+    with events around each call; the roofline counts, per product pass,
+    the head once plus each row's hidden row and noise row.  With ``unfused`` the LM head over every node (hipBLASLt bf16 GEMM
     to fp32 logits) followed by srt_accept is timed too, for comparison."""
     import torch
 
@@ -210,10 +248,11 @@ def fused_head(st, cfg, calls: int, unfused: bool):
     emitted = out["n_emitted"].cpu().numpy().astype(np.int64)
     levels = int(emitted.max())
     walkers = [int((emitted > l).sum()) for l in range(levels)]  # sequences walking at level l
-    per_level_head = V * dm * 2
-    nbytes = sum(per_level_head + n * (dm * 2 + (V * 4 if st.gumbel is not None else 0)) for n in walkers)
-    flops = sum(2.0 * n * dm * V for n in walkers)
-    res = {"ms": ms, "d_model": dm, "levels": levels, "walkers_per_level": walkers,
+    passes = head_passes(tree, out["out_nodes"].cpu().numpy(), emitted, cfg.max_depth)
+    row_bytes = dm * 2 + (V * 4 if st.gumbel is not None else 0)  # hidden row + noise row
+    nbytes = sum(V * dm * 2 + rows * row_bytes for rows in passes)  # the head once per pass
+    flops = sum(2.0 * rows * dm * V for rows in passes)
+    res = {"ms": ms, "d_model": dm, "levels": levels, "walkers_per_level": walkers, "rows_per_pass": passes,
            "mean_emitted": float(emitted.mean()),
            "roofline": {"bound": "hbm", "achieved": nbytes / (ms / 1e3) / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                         "frac": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, "algorithmic_bytes": float(nbytes),
