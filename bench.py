@@ -319,6 +319,7 @@ def main():
 
     import torch
 
+    from paper_2601_09083_amd import simulate as SIM
     from paper_2601_09083_amd import workload as W
     from paper_2601_09083_amd.pipeline import VerifyState
 
@@ -337,15 +338,30 @@ def main():
     cfg = W.CONFIGS[args.config]
     t_setup = time.perf_counter()
     n_steps = args.steps + args.warmup + args.part_steps + 4
-    st = VerifyState.build(cfg, steps_headroom=n_steps, kv_headroom=n_steps * (cfg.max_depth + 1))
-    st.draft()
-    st.make_logits(sampled=not args.greedy)
+    # running sequences follow their true continuations (mutated rollouts of
+    # their prompt, like every cached rollout); the target logits agree with
+    # those continuations, so each step drafts from where the last one left
+    sim = SIM.make_sim_tokens(cfg, future_len=(n_steps + 2) * (cfg.max_depth + 1))
+    st = VerifyState.build(cfg, tokens=sim.tokens, steps_headroom=n_steps, kv_headroom=n_steps * (cfg.max_depth + 1))
+    target = SIM.ContinuationTarget(st, sim.future, sampled=not args.greedy)
     torch.cuda.synchronize()
     t_setup = time.perf_counter() - t_setup
     print(f"# setup {t_setup:.1f}s: {cfg.name}, B={st.tokens.batch}", file=sys.stderr, flush=True)
+    step_no = [0]
 
+    def draft():
+        st.draft()
+        target.apply(st, step_no[0])
+        step_no[0] += 1
+
+    def accept():
+        st.accept()
+        target.advance(st)
+
+    calls = {"draft": draft, "attention": st.attention, "accept": accept, "insert": st.insert, "commit": st.commit}
     for _ in range(args.warmup):
-        st.step()
+        for p in ("draft", "attention", "accept", "insert", "commit"):
+            calls[p]()
     torch.cuda.synchronize()
 
     parts = ("draft", "attention", "accept", "insert", "commit")
@@ -364,14 +380,14 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        st.draft()
+        draft()
         attn_ev[k][0].record(stream)
         st.attention()
         attn_ev[k][1].record(stream)
         rec_len[k, 0].copy_(st.attn_len)
         rec_len[k, 1].copy_(st.tree["n_nodes"])
         rec_depth[k].copy_(st.tree["tree_depth"])
-        st.accept()
+        accept()
         rec_emit[k].copy_(st.acc["n_emitted"])
         st.insert()
         st.commit()
@@ -388,6 +404,11 @@ def main():
             part_ev[k][j][0].record(stream)
             getattr(st, p)()
             part_ev[k][j][1].record(stream)
+            if p == "draft":
+                target.apply(st, step_no[0])
+                step_no[0] += 1
+            elif p == "accept":
+                target.advance(st)
     torch.cuda.synchronize()
     part_ms = {p: float(np.mean([part_ev[k][j][0].elapsed_time(part_ev[k][j][1]) for k in range(args.part_steps)]))
                for j, p in enumerate(parts)} if args.part_steps > 0 else {}
@@ -433,7 +454,8 @@ def main():
             "workload": (f"{cfg.name}: {st.tokens.batch} sequences, Hq {cfg.hq}/Hkv {cfg.hkv}/d {cfg.head_dim}, "
                          f"contexts {cfg.ctx_len.kind}({cfg.ctx_len.a},{cfg.ctx_len.b}), draft trees N={cfg.n_nodes} "
                          f"Dmax={cfg.max_depth}, vocab {cfg.vocab}, "
-                         f"{'greedy' if args.greedy else 'T=1 Gumbel'} acceptance, caches of "
+                         f"{'greedy' if args.greedy else 'T=1 Gumbel'} acceptance against a target that follows each "
+                         f"sequence's continuation, caches of "
                          f"{cfg.rollouts_per_prompt} prior rollouts/prompt"),
             "global_batch": st.tokens.batch,
             "seq_len": int(st.tokens.ctx_len.max()),

@@ -84,6 +84,58 @@ def make_sim_tokens(cfg: W.Config, future_len: int, runahead_per_prompt: int = 4
     return SimTokens(tw, future, runahead)
 
 
+class ContinuationTarget:
+    """Per-step logits and Gumbel noise for a decode loop in which every
+    running sequence follows its true continuation (``SimTokens.future``).
+
+    The logits are fixed random N(0, sigma) rows [B, N, V] plus ``boost`` at
+    each node's continuation token -- the token depth(u) positions past what
+    the sequence has committed -- written in place each step and restored to
+    the saved values the next, so the walk accepts exactly the drafted path
+    that agrees with the continuation and the bonus token continues it.  The
+    noise is read at a step-dependent offset of a buffer one sequence larger
+    than [B, Dmax+1, V], so consecutive steps see different noise without new
+    draws.  All of it is a stand-in for the policy (no part of the method)."""
+
+    def __init__(self, st, future: np.ndarray, boost: float = 100.0, sampled: bool = True, seed: int = 4321):
+        cfg, B, dev = st.cfg, st.tokens.batch, st.device
+        N, V, D1 = cfg.n_nodes, cfg.vocab, cfg.max_depth + 1
+        none = np.full((B, N), -1, dtype=np.int32)
+        self.logits = W.make_logits(cfg, none, none, np.ones(B, dtype=np.int32), device=dev, seed=seed,
+                                    boost="none")
+        self.noise = W.make_gumbel(cfg, B + 1, device=dev, seed=seed + 1) if sampled else None
+        self.future = torch.as_tensor(future, device=dev).long()
+        self.used = torch.zeros(B, dtype=torch.int64, device=dev)
+        self.rowbase = (torch.arange(B * N, device=dev, dtype=torch.int64) * V).view(B, N)
+        self.flat = None
+        self.saved = None
+        self.boost = float(boost)
+        self.shape = (B, D1, V)
+
+    def apply(self, st, step: int):
+        """Logits and noise for the trees just drafted (call after draft)."""
+        flat_l = self.logits.view(-1)
+        if self.flat is not None:
+            flat_l[self.flat] = self.saved
+        depth = st.tree["tree_depth"].long().clamp(min=0)
+        pos = (self.used[:, None] + depth).clamp(max=self.future.shape[1] - 1)
+        tok = torch.gather(self.future, 1, pos)
+        self.flat = (self.rowbase + tok).view(-1)
+        self.saved = flat_l[self.flat]
+        flat_l[self.flat] = self.saved + self.boost
+        st.logits = self.logits
+        if self.noise is not None:
+            B, D1, V = self.shape
+            off = (step * 104729) % (D1 * V)
+            st.gumbel = self.noise.view(-1)[off: off + B * D1 * V].view(B, D1, V)
+        else:
+            st.gumbel = None
+
+    def advance(self, st):
+        """Account the tokens the step emitted (call after accept)."""
+        self.used += st.acc["n_emitted"].long()
+
+
 def run(cfg: W.Config, sim: SimTokens, steps: int, strategy: str = "onthefly", alpha: float = 0.0,
         min_score: float = 0.0, chain: bool = False, n_nodes: Optional[int] = None, device: str = "cuda") -> Dict:
     """One simulation: ``strategy`` is "history" (prior rollouts only, no
