@@ -290,6 +290,47 @@ def fused_head(st, cfg, calls: int, unfused: bool):
     return res
 
 
+def runahead_inserts(cfg, st, sim, n_steps: int):
+    """Per-step run-ahead continuations for configurations that insert them
+    (the long-tail regime): step k inserts cfg.runahead_streams new streams
+    of cfg.runahead_len tokens, stream j a fresh mutation of the next window
+    of its sequence's base (sequence j mod B), as run-ahead rollouts that
+    generate past the current position would be.  Returns a function that
+    performs step k's insertion on the device, or None."""
+    import torch
+
+    from paper_2601_09083_amd import srt
+    from paper_2601_09083_amd import workload as W
+
+    R, Lr = cfg.runahead_streams, cfg.runahead_len
+    if R <= 0 or Lr <= 0:
+        return None
+    tw = sim.tokens
+    B = tw.batch
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(5150 + cfg.index)))
+    toks = np.zeros((n_steps, R, Lr), dtype=np.int32)
+    lens = np.zeros((n_steps, R), dtype=np.int32)
+    prompts = np.array([int(tw.seq_prompt[j % B]) for j in range(R)], dtype=np.int32)
+    for k in range(n_steps):
+        for j in range(R):
+            base = tw.bases[int(prompts[j])]
+            start = (int(tw.ctx_len[j % B]) + k * Lr) % max(1, base.shape[0] - Lr)
+            r = W.mutate(rng, base[start:start + Lr], vocab=cfg.vocab, p_sub=cfg.p_sub, p_del=cfg.p_del,
+                         p_ins=cfg.p_ins)[:Lr]
+            toks[k, j, :r.shape[0]] = r
+            lens[k, j] = r.shape[0]
+    ids = st.caches.new_streams(n_steps * R).reshape(n_steps, R)
+    dev = st.attn_len.device
+    t_toks = torch.as_tensor(toks, device=dev)
+    t_lens = torch.as_tensor(lens, device=dev)
+    t_ids = torch.as_tensor(ids, device=dev)
+    t_prompts = torch.as_tensor(prompts, device=dev)
+
+    def insert(k):
+        srt.srt_trie_insert(st.caches.ws, t_prompts, t_ids[k], t_toks[k], t_lens[k])
+    return insert
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -358,7 +399,16 @@ def main():
         st.accept()
         target.advance(st)
 
-    calls = {"draft": draft, "attention": st.attention, "accept": accept, "insert": st.insert, "commit": st.commit}
+    ra_insert = runahead_inserts(cfg, st, sim, n_steps)
+    ins_no = [0]
+
+    def insert():
+        st.insert()
+        if ra_insert is not None:  # run-ahead continuations of this step
+            ra_insert(ins_no[0])
+            ins_no[0] += 1
+
+    calls = {"draft": draft, "attention": st.attention, "accept": accept, "insert": insert, "commit": st.commit}
     for _ in range(args.warmup):
         for p in ("draft", "attention", "accept", "insert", "commit"):
             calls[p]()
@@ -389,7 +439,7 @@ def main():
         rec_depth[k].copy_(st.tree["tree_depth"])
         accept()
         rec_emit[k].copy_(st.acc["n_emitted"])
-        st.insert()
+        insert()
         st.commit()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -402,7 +452,7 @@ def main():
     for k in range(args.part_steps):
         for j, p in enumerate(parts):
             part_ev[k][j][0].record(stream)
-            getattr(st, p)()
+            (insert if p == "insert" else getattr(st, p))()
             part_ev[k][j][1].record(stream)
             if p == "draft":
                 target.apply(st, step_no[0])
@@ -456,7 +506,9 @@ def main():
                          f"Dmax={cfg.max_depth}, vocab {cfg.vocab}, "
                          f"{'greedy' if args.greedy else 'T=1 Gumbel'} acceptance against a target that follows each "
                          f"sequence's continuation, caches of "
-                         f"{cfg.rollouts_per_prompt} prior rollouts/prompt"),
+                         f"{cfg.rollouts_per_prompt} prior rollouts/prompt"
+                         + (f", {cfg.runahead_streams} run-ahead continuations of {cfg.runahead_len} tokens "
+                            f"inserted per step" if ra_insert is not None else "")),
             "global_batch": st.tokens.batch,
             "seq_len": int(st.tokens.ctx_len.max()),
             "mean_ctx": float(st.tokens.ctx_len.mean()),

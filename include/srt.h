@@ -175,10 +175,13 @@ int srt_draft(const void* ws, int32_t B, const int32_t* prompt_ids, const int32_
  * scratch: device buffer, 256-byte aligned, of at least
  * srt_tree_attn_scratch_bytes(...) bytes (always > 0): the work list the
  * call builds for its own kernels, plus split-context partial results when
- * a context can exceed one 8192-key split.  Owned by the caller; contents
- * are overwritten; calls that share a scratch buffer must not overlap.
+ * a context can exceed one split.  A split is 8192 keys, or a smaller power
+ * of two (down to 1024) when B * Hkv is small, chosen from B, Hkv, page and
+ * max_pages alone (the results do not depend on it beyond fp32 rounding).
+ * Owned by the caller; contents are overwritten; calls that share a
+ * scratch buffer must not overlap.
  * Unsupported (SRT_ERR_UNSUPPORTED): B > 65535, Hkv > 255, max_pages *
- * page beyond 4095 splits of 8192 keys, or N * Hq / Hkv / 256 > 2046.
+ * page beyond 4095 splits, or N * Hq / Hkv / 256 > 2046.
  * ---------------------------------------------------------------------- */
 size_t srt_tree_attn_scratch_bytes(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d,
                                    int32_t page, int32_t max_pages);

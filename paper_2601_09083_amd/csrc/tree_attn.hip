@@ -63,7 +63,8 @@ constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
 constexpr int kTile = 64;                  // keys per tile
 constexpr int kSubRows = kTile / kWaves;   // keys of each tile one wave stages
 constexpr int kMaxN = 256;                 // tree rows
-constexpr int kChunk = 8192;               // keys per split
+constexpr int kChunk = 8192;               // keys per split, at most (the split size is chosen per call)
+constexpr int kMinChunk = 1024;            // keys per split, at least
 
 struct AttnArgs {
   const uint16_t* q;
@@ -83,6 +84,7 @@ struct AttnArgs {
   int64_t num_pages;
   float scale_log2;
   int32_t S, RB, total;
+  int32_t chunk;  // keys per split: a power of two in [kMinChunk, kChunk]
 };
 
 // Work list: plan[0] = number of items, plan[1] = next item to hand out,
@@ -192,10 +194,10 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   const SeqInfo si = seq_info(a, b);
   const int rows = si.n * a.G;
   if (rb * kRowsPerBlock >= rows) return;
-  const int k_begin = s * kChunk;
+  const int k_begin = s * a.chunk;
   if (k_begin >= si.total) return;
-  const int k_end = min(k_begin + kChunk, si.total);
-  const int nsplit = (si.total + kChunk - 1) / kChunk;
+  const int k_end = min(k_begin + a.chunk, si.total);
+  const int nsplit = (si.total + a.chunk - 1) / a.chunk;
   const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
   const int row0 = rb * kRowsPerBlock + w * kRowsPerWave;
   const bool wave_active = row0 < rows;  // wave-uniform
@@ -266,7 +268,7 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   // Page ids of this wave's sub-block of every tile of the split, one tile
   // per lane and register (a split has 128 tiles), fetched once; the loop
   // reads them with v_readlane and touches no block-table memory.
-  static_assert(kChunk / kTile == 2 * SRT_WAVE, "two registers of page ids per split");
+  static_assert(kChunk / kTile == 2 * SRT_WAVE, "two registers of page ids per split (of at most kChunk keys)");
   int pg_lane[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -555,10 +557,10 @@ __global__ __launch_bounds__(1024) void tree_attn_plan_kernel(AttnArgs a) {
     const SeqInfo si = seq_info(a, b);
     const int rows = si.n * a.G;
     const int rbs = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
-    const int full = si.total / kChunk;
-    const int tail = si.total - full * kChunk;
+    const int full = si.total / a.chunk;
+    const int tail = si.total - full * a.chunk;
     const int waves = min(kWaves, (rows + kRowsPerWave - 1) / kRowsPerWave);
-    if (full > 0) f(plan_key(kChunk / kTile, waves), 0, full, rbs);
+    if (full > 0) f(plan_key(a.chunk / kTile, waves), 0, full, rbs);
     if (tail > 0) f(plan_key((tail + kTile - 1) / kTile, waves), full, 1, rbs);
   };
   for (int b = tid; b < a.B; b += 1024)
@@ -589,7 +591,7 @@ __global__ __launch_bounds__(1024) void tree_attn_plan_kernel(AttnArgs a) {
   // combine units: 8-row groups of every (sequence, KV head) with several splits
   for (int b = tid; b < a.B; b += 1024) {
     const SeqInfo si = seq_info(a, b);
-    if (si.total <= kChunk) continue;
+    if (si.total <= a.chunk) continue;
     const int groups = (si.n * a.G + 7) / 8;
     int u = atomicAdd(&ncomb, groups * a.Hkv);
     for (int g = 0; g < a.Hkv; ++g)
@@ -629,7 +631,7 @@ __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
     const int bg = a.plan[a.combine_at + u];
     const int b = bg & 0xffff, g = bg >> 16;
     const SeqInfo si = seq_info(a, b);
-    const int nsplit = (si.total + kChunk - 1) / kChunk;
+    const int nsplit = (si.total + a.chunk - 1) / a.chunk;
     const int rows = si.n * a.G;
     for (int sub = threadIdx.x; sub < 8 * Q; sub += 256) {
       const int r = a.plan[a.combine_at + a.max_units + u] * 8 + sub / Q, q = sub % Q;
@@ -661,9 +663,21 @@ __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
   }
 }
 
-int splits_for(int32_t page, int32_t max_pages) {
+// Keys per split: the largest power of two in [kMinChunk, kChunk] that still
+// gives B * Hkv * RB * (capacity / chunk) >= 512 work items (two per CU of
+// the 256; RB row blocks per sequence and KV head), so that small batches
+// of long contexts are split over enough workgroups; large batches and wide
+// trees keep 8192-key splits (fewer partial results).
+int chunk_for(int32_t B, int32_t Hkv, int64_t RB, int32_t page, int32_t max_pages) {
   const int64_t cap = static_cast<int64_t>(page) * max_pages;
-  return static_cast<int>((cap + kChunk - 1) / kChunk);
+  int chunk = kChunk;
+  while (chunk > kMinChunk && static_cast<int64_t>(B) * Hkv * RB * ((cap + chunk - 1) / chunk) < 512) chunk /= 2;
+  return chunk;
+}
+
+int splits_for(int32_t page, int32_t max_pages, int chunk) {
+  const int64_t cap = static_cast<int64_t>(page) * max_pages;
+  return static_cast<int>((cap + chunk - 1) / chunk);
 }
 
 // Combine units (8-row groups) needed at most.
@@ -693,9 +707,9 @@ int cu_count() {
 extern "C" size_t srt_tree_attn_scratch_bytes(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d, int32_t page,
                                               int32_t max_pages) {
   if (B < 0 || N < 1 || N > kMaxN || Hq < 1 || Hkv < 1 || Hq % Hkv || page < 1 || max_pages < 1) return 0;
-  const int S = splits_for(page, max_pages);
   const int G = Hq / Hkv;
   const int64_t RB = (N * G + kRowsPerBlock - 1) / kRowsPerBlock;
+  const int S = splits_for(page, max_pages, chunk_for(B, Hkv, RB, page, max_pages));
   const size_t plan = plan_bytes(static_cast<int64_t>(B) * Hkv * S * RB, max_combine_units(B, N, G, Hkv));
   if (S <= 1) return plan;
   return plan + static_cast<size_t>(B) * Hkv * S * RB * kRowsPerBlock * (d + 2) * sizeof(float);
@@ -713,7 +727,8 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
   if (page < 16 || (page & (page - 1))) return SRT_ERR_UNSUPPORTED;
   // work-list packing: sequence < 65536, KV head < 256, split < 4096,
   // row block < 2048, combine units < 2^31
-  if (B > 65535 || Hkv > 255 || splits_for(page, max_pages) > 4095 || (N * (Hq / Hkv)) / kRowsPerBlock > 2046 ||
+  const int chunk = chunk_for(B, Hkv, (N * (Hq / Hkv) + kRowsPerBlock - 1) / kRowsPerBlock, page, max_pages);
+  if (B > 65535 || Hkv > 255 || splits_for(page, max_pages, chunk) > 4095 || (N * (Hq / Hkv)) / kRowsPerBlock > 2046 ||
       max_combine_units(B, N, Hq / Hkv, Hkv) > (int64_t(1) << 30))
     return SRT_ERR_UNSUPPORTED;
   if (B == 0) return SRT_OK;
@@ -742,7 +757,8 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
   a.max_pages = max_pages;
   a.num_pages = num_pages;
   a.scale_log2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
-  a.S = splits_for(page, max_pages);
+  a.chunk = chunk;
+  a.S = splits_for(page, max_pages, chunk);
   a.RB = (N * a.G + kRowsPerBlock - 1) / kRowsPerBlock;
   const int64_t total = static_cast<int64_t>(B) * Hkv * a.S * a.RB;
   if (total > (int64_t(1) << 30)) return SRT_ERR_INVALID;

@@ -76,12 +76,22 @@ def test_shapes_ragged(d, hq, hkv):
 
 
 def test_split_contexts_and_combine():
-    # contexts longer than one split (8192 keys) exercise the partial + combine
-    # path; lengths sit on and around split and tile boundaries
+    # contexts longer than one split exercise the partial + combine path; a
+    # batch this small gets 1024-key splits, and the lengths sit on and
+    # around split (1024 and 8192) and tile boundaries
     say("attn: split contexts")
     ctx = [4088, 8192 - 64 - 7, 8192 - 64, 8192, 9000, 12345, 16384 - 30, 25000, 100]
     c = Case(11, len(ctx), 64, 28, 4, 128, ctx)
     c.check(c.run())
+
+
+def test_split_contexts_8192_key_splits():
+    # B * Hkv = 256 with 16k-key capacity keeps the largest (8192-key) splits
+    say("attn: 8192-key splits")
+    base = [8192 - 64 - 7, 8192, 9000, 12345, 16354, 100, 5000, 8193]
+    ctx = [base[i % len(base)] for i in range(32)]
+    c = Case(31, len(ctx), 4, 8, 8, 128, ctx)
+    c.check(c.run(), seqs=[0, 1, 2, 3, 4, 5, 6, 7, 12, 20])
 
 
 def test_split_contexts_d64():
