@@ -93,7 +93,7 @@ __global__ void create_roots_kernel(void* ws, int32_t n_prompts) {
   if (p < n_prompts) t.roots[p] = trie_get_or_create(t, kRootParent, static_cast<uint32_t>(p));
 }
 
-__global__ __launch_bounds__(256) void insert_kernel(void* ws, const int32_t* __restrict__ prompt_ids,
+__global__ __launch_bounds__(1024) void insert_kernel(void* ws, const int32_t* __restrict__ prompt_ids,
                                                      const int32_t* __restrict__ stream_ids,
                                                      const int32_t* __restrict__ tokens,
                                                      const int32_t* __restrict__ lengths, int32_t stride) {
@@ -348,7 +348,12 @@ int srt_trie_insert(void* ws, int32_t n, const int32_t* prompt_ids, const int32_
   if (!ws || n < 0 || stride < 1) return SRT_ERR_INVALID;
   if (n == 0) return SRT_OK;
   if (!prompt_ids || !stream_ids || !tokens || !lengths) return SRT_ERR_INVALID;
-  insert_kernel<<<n, 256, 0, as_stream(stream)>>>(ws, prompt_ids, stream_ids, tokens, lengths, stride);
+  // one thread per substring start (up to 63 starts before the segment plus
+  // one per token), so a segment of up to ~960 tokens walks its chains in
+  // a single round of at most D dependent steps
+  const int64_t starts = static_cast<int64_t>(stride) + 63;
+  const unsigned threads = static_cast<unsigned>(std::min<int64_t>(1024, (starts + 63) / 64 * 64));
+  insert_kernel<<<n, threads, 0, as_stream(stream)>>>(ws, prompt_ids, stream_ids, tokens, lengths, stride);
   return launch_status();
 }
 
