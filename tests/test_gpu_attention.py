@@ -94,6 +94,17 @@ def test_split_contexts_8192_key_splits():
     c.check(c.run(), seqs=[0, 1, 2, 3, 4, 5, 6, 7, 12, 20])
 
 
+@pytest.mark.parametrize("B,split", [(16, 4096), (8, 2048)])
+def test_split_contexts_mid_size_splits(B, split):
+    # B * Hkv = 128 / 64 with 16k-key capacity: the call picks 4096- / 2048-key
+    # splits; lengths on and around those boundaries
+    say(f"attn: {split}-key splits")
+    base = [split - 1, split, split + 1, 2 * split - 64, 3 * split + 5, 16000, 100, 7]
+    ctx = [base[i % len(base)] for i in range(B)]
+    c = Case(37 + B, B, 8, 8, 8, 128, ctx)
+    c.check(c.run(), seqs=list(range(len(base))))
+
+
 def test_split_contexts_d64():
     say("attn: split contexts, d=64")
     ctx = [8200, 17000, 3]
