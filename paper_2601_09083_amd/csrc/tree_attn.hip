@@ -32,10 +32,12 @@
 //     on tiles that reach the tree positions or the end of the range each
 //     row takes a 64-bit visibility window of it (two LDS words) and masks
 //     its scores bit by bit.
-//   * Long contexts are split into fixed chunks of keys so the grid has
-//     enough independent work; each split writes unnormalised partial
-//     output plus (max, sum) and a small combine kernel merges them.  A
-//     sequence that fits in one chunk writes bf16 output directly.
+//   * Long contexts are split into chunks of keys so the grid has enough
+//     independent work (8192 keys, or a smaller power of two down to 1024
+//     when the batch has few sequences and KV heads); each split writes
+//     unnormalised partial output plus (max, sum) and a small combine
+//     kernel merges them.  A sequence that fits in one split writes bf16
+//     output directly.
 //   * Work is scheduled by a small plan kernel that lists the (sequence, KV
 //     head, split, row block) items that have work, longest first; one
 //     persistent workgroup per CU takes items from an atomic counter, so no
