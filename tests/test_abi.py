@@ -51,6 +51,38 @@ def test_scratch_bytes():
     assert S.srt_tree_attn_scratch_bytes(4, 8, 5, 2, 64, 16, 40) == 0  # Hq % Hkv != 0
 
 
+def _expected_attn_scratch(B, N, Hq, Hkv, d, page, max_pages):
+    """The scratch size srt_tree_attn documents: its work list (a 64-int
+    header, two int32 per (sequence, KV head, split, row block) item and per
+    8-row combine unit), plus fp32 partial rows and (max, sum) pairs when a
+    context can span several splits.  A split is the largest power of two in
+    [1024, 8192] keys that keeps B * Hkv * row blocks * splits >= 512."""
+    G = Hq // Hkv
+    rb = -(-(N * G) // 256)
+    cap = page * max_pages
+    chunk = 8192
+    while chunk > 1024 and B * Hkv * rb * (-(-cap // chunk)) < 512:
+        chunk //= 2
+    S = -(-cap // chunk)
+    items = B * Hkv * S * rb
+    units = B * Hkv * (-(-(N * G) // 8))
+    plan = -(-((64 + 2 * items + 2 * units) * 4) // 256) * 256
+    return plan if S <= 1 else plan + B * Hkv * S * rb * 256 * (d + 2) * 4, chunk
+
+
+@pytest.mark.parametrize("shape,chunk", [
+    ((64, 32, 12, 2, 128, 16, 288), 1024),    # 1.5B-shaped batch: small, short contexts
+    ((16, 8, 8, 8, 128, 16, 1001), 4096),
+    ((8, 8, 8, 8, 128, 16, 1001), 2048),
+    ((256, 64, 28, 4, 128, 16, 2052), 8192),  # 7B-shaped batch
+    ((8, 256, 28, 4, 128, 16, 2100), 8192),   # long-tail: seven row blocks keep large splits
+])
+def test_scratch_bytes_follow_the_split_rule(shape, chunk):
+    want, got_chunk = _expected_attn_scratch(*shape)
+    assert got_chunk == chunk
+    assert S.srt_tree_attn_scratch_bytes(*shape) == want
+
+
 def test_host_validation_before_any_hip_call():
     L = S.lib()
     cfg = S.TrieConfig(4, 8, 12, 0, 100)
