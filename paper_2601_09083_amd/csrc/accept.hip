@@ -165,13 +165,11 @@ __device__ inline Best chunk_argmax(const AcceptArgs& a, const float* __restrict
   return b;
 }
 
-// Level counters: every sequence walks at level 0, none yet at later ones.
-__global__ __launch_bounds__(128) void accept_reset_kernel(AcceptArgs a) {
-  for (int i = threadIdx.x; i <= kMaxLevels; i += blockDim.x) a.n_act[i] = i == 0 ? a.B : 0;
-}
-
-// Outputs to -1; sequence b walks from its root.
+// Outputs to -1; sequence b walks from its root; level counters: every
+// sequence walks at level 0, none yet at later ones (block 0).
 __global__ __launch_bounds__(256) void accept_init_kernel(AcceptArgs a) {
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i <= kMaxLevels; i += 256) a.n_act[i] = i == 0 ? a.B : 0;
   const int b = blockIdx.x * 256 + threadIdx.x;
   if (b >= a.B) return;
   const int64_t row = static_cast<int64_t>(b) * (a.Dmax + 1);
@@ -287,12 +285,8 @@ extern "C" int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const f
   if (grid > 0x7FFFFFFF) return SRT_ERR_UNSUPPORTED;
 
   hipStream_t s = as_stream(stream);
-  accept_reset_kernel<<<1, 128, 0, s>>>(a);
+  accept_init_kernel<<<(B + 255) / 256, 256, 0, s>>>(a);
   int st = launch_status();
-  if (st == SRT_OK) {
-    accept_init_kernel<<<(B + 255) / 256, 256, 0, s>>>(a);
-    st = launch_status();
-  }
   const unsigned walk_grid = static_cast<unsigned>((B + kWalkWaves - 1) / kWalkWaves);
   for (int level = 0; level <= Dmax && st == SRT_OK; ++level) {
     if (gumbel)
