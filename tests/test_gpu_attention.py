@@ -105,6 +105,16 @@ def test_split_contexts_mid_size_splits(B, split):
     c.check(c.run(), seqs=list(range(len(base))))
 
 
+@pytest.mark.parametrize("page,d", [(32, 128), (64, 128), (64, 64)])
+def test_larger_pages(page, d):
+    # pages of 32 and 64 tokens: a 64-key tile spans two or one page, ragged
+    # tails and split contexts included
+    say(f"attn: page {page}, d={d}")
+    ctx = [0, 31, 32, 33, 63, 64, 65, 1000, 9000, 4097]
+    c = Case(43 + page, len(ctx), 16, 8, 2, d, ctx, page=page)
+    c.check(c.run())
+
+
 def test_split_contexts_d64():
     say("attn: split contexts, d=64")
     ctx = [8200, 17000, 3]
