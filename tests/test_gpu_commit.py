@@ -3,7 +3,8 @@ draft tail advanced) against oracle/commit.py, bit-exact.
 
 * random caches with paths that overlap their own destinations (node c_i = j
   for i < j), identity paths, empty paths, paths of Dmax nodes, short and
-  empty draft tails, d = 64 / 128, one to four KV heads; the whole cache
+  empty draft tails, d = 64 / 128, one to four KV heads, pages of 1, 16, 32
+  and 64 tokens; the whole cache
   (including pages of other sequences and unused pages) is compared;
 * the tiny configuration run as a real decode loop for three steps: each
   step's draft is checked against the oracle drafting from the grown
@@ -44,11 +45,11 @@ def bits(t):
     return t.view(torch.int16).cpu().numpy()
 
 
-@pytest.mark.parametrize("d,Hkv", [(64, 1), (128, 4), (128, 2)])
-def test_commit_random(d, Hkv):
-    say(f"commit random d={d} Hkv={Hkv}")
-    rng = np.random.default_rng(100 * d + Hkv)
-    B, N, page, Dmax, Qmax = 9, 24, 16, 6, 5
+@pytest.mark.parametrize("d,Hkv,page", [(64, 1, 16), (128, 4, 16), (128, 2, 16), (128, 2, 32), (64, 3, 64), (128, 1, 1)])
+def test_commit_random(d, Hkv, page):
+    say(f"commit random d={d} Hkv={Hkv} page={page}")
+    rng = np.random.default_rng(100 * d + Hkv + 7 * page)
+    B, N, Dmax, Qmax = 9, 24, 6, 5
     L = rng.integers(0, 120, B).astype(np.int32)
     L[0] = 0
     pages_per = (L + N + page - 1) // page
