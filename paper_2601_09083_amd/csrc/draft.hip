@@ -24,7 +24,15 @@
 // relative order when a node is added.  A frontier bounded at twice the node
 // budget is exact: when it overflows, the worst of more than `budget`
 // candidates is dropped, and it could never be selected.
+//
+// Tree drafts take a faster route first: a level-synchronous expansion that
+// walks the child lists of many candidates at once (one list per lane) and
+// orders the result once at the end (see draft_levels).  It gives the same
+// tree; a sequence whose candidates overflow its LDS pool falls back to the
+// one-at-a-time selection above, which also serves chain drafts.
 #include <cmath>
+#include <cstdint>
+#include <type_traits>
 
 #include "common.h"
 
@@ -107,6 +115,350 @@ __device__ inline int wave_sum_i(int v) {
 __device__ inline Key frontier_key(const Smem& sm, int e) {
   const int par = sm.f_par[e];
   return make_key(sm.f_score[e], sm.sel_depth[par] + 1, sm.sel_rank[par], sm.f_tok[e], e);
+}
+
+// ---------------------------------------------------------------------------
+// Level-synchronous expansion (tree drafts).
+//
+// The selected nodes are the `budget` best candidates under the total order,
+// and no node ranks above its parent (its score is at most the parent's, its
+// depth larger).  So the candidates can be discovered a level at a time: keep
+// a pool of discovered candidates and, in each round, expand every pool entry
+// not yet expanded that has fewer than `budget` entries of strictly larger
+// score.  When a round finds no such entry the pool holds the best `budget`
+// candidates: an undiscovered candidate v has a discovered ancestor a that was
+// never expanded, so at least `budget` candidates score strictly above a and
+// therefore rank strictly above v.  Each round adds the next level of the
+// final tree, so the rounds follow the tree depth rather than the node count.
+// The order itself (lexicographic token paths break ties) is computed once at
+// the end.  Entries that cannot be selected are dropped as they are found; a
+// round whose children do not fit the pool reports failure.
+// ---------------------------------------------------------------------------
+constexpr int kPool = 1024;     // candidate pool entries (entry 0 is u)
+constexpr uint8_t kOpen = 0;    // discovered, children not yet walked
+constexpr uint8_t kDone = 1;    // children walked, or a leaf, or at the depth limit
+constexpr uint8_t kDropped = 2; // cannot be selected
+constexpr int64_t kNoKey = INT64_MAX;
+
+struct Pool {
+  double score[kPool];            // path product; -1 below the score threshold
+  unsigned long long num[kPool];  // own count until scored, then the children's count sum; scratch at the end
+  uint32_t first[kPool];          // child-list head
+  int32_t tok[kPool];
+  uint16_t par[kPool];
+  uint16_t aux[kPool];            // compaction map, then rank of the token path among its depth
+  uint16_t pos[kPool];            // slot within its depth, then position in the selection order
+  uint16_t list[kPool];           // entries to expand; then all entries, by depth
+  uint8_t depth[kPool];
+  uint8_t state[kPool];
+  uint32_t dcount[64];            // entries per depth
+  uint32_t dstart[64];            // first list slot of each depth
+  uint32_t m;                     // entries in use; appends reserve slots here
+};
+
+__device__ inline int rank_below(uint64_t bal) {
+  return static_cast<int>(__builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(bal >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bal), 0u)));
+}
+
+// Scores as signed integers: ordered like the (non-negative) scores, with the
+// -1 of an entry below the score threshold under all of them.
+__device__ inline int64_t score_key(double s) { return __double_as_longlong(s); }
+
+// Runs f with a compile-time number of 64-entry chunks per lane covering n
+// entries (n <= kPool).
+template <typename F>
+__device__ inline auto by_chunks(int n, F f) {
+  if (n <= SRT_WAVE) return f(std::integral_constant<int, 1>{});
+  if (n <= 2 * SRT_WAVE) return f(std::integral_constant<int, 2>{});
+  if (n <= 4 * SRT_WAVE) return f(std::integral_constant<int, 4>{});
+  if (n <= 8 * SRT_WAVE) return f(std::integral_constant<int, 8>{});
+  return f(std::integral_constant<int, kPool / SRT_WAVE>{});
+}
+
+// c[r] += the number of entries w in 1 .. M-1 ranking strictly above key r:
+// a larger score or, with kTies, an equal score and a larger tie key (num).
+// Each entry is read from LDS once and compared with all R keys held here.
+template <int R, bool kTies>
+__device__ inline void count_above(const Pool& P, int M, const int64_t (&ks)[R], const uint32_t (&kt)[R],
+                                   int (&c)[R]) {
+#pragma unroll 4
+  for (int w = 1; w < M; ++w) {
+    const int64_t sw = score_key(P.score[w]);
+    const uint32_t tw = kTies ? static_cast<uint32_t>(P.num[w]) : 0u;
+#pragma unroll
+    for (int r = 0; r < R; ++r) c[r] += static_cast<int>((sw > ks[r]) | (kTies & (sw == ks[r]) & (tw > kt[r])));
+  }
+}
+
+// Drops the n listed open entries that have `budget` or more entries of
+// strictly larger score, and compacts the list; returns its new length.
+template <int R>
+__device__ int drop_listed(Pool& P, int lane, int M, int n, int budget) {
+  int idx[R], c[R];
+  int64_t ks[R];
+  uint32_t kt[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int j = lane + SRT_WAVE * r;
+    idx[r] = j < n ? P.list[j] : -1;
+    ks[r] = idx[r] >= 0 ? score_key(P.score[idx[r]]) : kNoKey;
+    kt[r] = 0;
+    c[r] = 0;
+  }
+  count_above<R, false>(P, M, ks, kt, c);
+  __syncthreads();  // every lane has read the list
+  int kept = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const bool keep = idx[r] >= 0 && c[r] < budget;
+    const uint64_t bal = __ballot(keep);
+    if (keep) P.list[kept + rank_below(bal)] = static_cast<uint16_t>(idx[r]);
+    else if (idx[r] >= 0) P.state[idx[r]] = kDropped;
+    kept += __popcll(bal);
+  }
+  return kept;
+}
+
+// Marks for keeping entry 0 and every entry that can still be selected (not
+// dropped, fewer than `budget` entries of strictly larger score), drops the
+// rest, and writes each kept entry's new index to aux; returns the count.
+template <int R>
+__device__ int keep_marks(Pool& P, int lane, int M, int budget) {
+  int c[R];
+  int64_t ks[R];
+  uint32_t kt[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = lane + SRT_WAVE * r;
+    const bool live = i >= 1 && i < M && P.state[i] != kDropped;
+    ks[r] = live ? score_key(P.score[i]) : kNoKey;
+    kt[r] = 0;
+    c[r] = 0;
+  }
+  count_above<R, false>(P, M, ks, kt, c);
+  int kept = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = lane + SRT_WAVE * r;
+    const bool keep = i == 0 || (i < M && ks[r] != kNoKey && c[r] < budget);
+    if (i < M && !keep) P.state[i] = kDropped;
+    const uint64_t bal = __ballot(keep);
+    if (keep) P.aux[i] = static_cast<uint16_t>(kept + rank_below(bal));
+    kept += __popcll(bal);
+  }
+  return kept;
+}
+
+// Position of every entry 1 .. M-1 in the selection order, from its score and
+// the tie key in num.
+template <int R>
+__device__ void positions(Pool& P, int lane, int M) {
+  int c[R];
+  int64_t ks[R];
+  uint32_t kt[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = lane + SRT_WAVE * r;
+    const bool v = i >= 1 && i < M;
+    ks[r] = v ? score_key(P.score[i]) : kNoKey;
+    kt[r] = v ? static_cast<uint32_t>(P.num[i]) : ~0u;
+    c[r] = 0;
+  }
+  count_above<R, true>(P, M, ks, kt, c);
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = lane + SRT_WAVE * r;
+    if (i >= 1 && i < M) P.pos[i] = static_cast<uint16_t>(c[r]);
+  }
+}
+
+// Keeps entry 0 and every entry that can still be selected, moved down in
+// index order.  A kept entry's parent is kept too (it scores at least as
+// high), and stays ahead of it.  Returns the new entry count.
+__device__ __forceinline__ int compact(Pool& P, int lane, int M, int budget) {
+  const int kept = by_chunks(M, [&](auto rc) { return keep_marks<decltype(rc)::value>(P, lane, M, budget); });
+  __syncthreads();
+  if (kept < M) {
+    // chunk by chunk: a chunk's new indices lie below its own range and above
+    // every index already written
+    for (int base = 0; base < M; base += SRT_WAVE) {
+      const int i = base + lane;
+      const bool keep = i < M && P.state[i] != kDropped;
+      double sc = 0.0;
+      unsigned long long nu = 0;
+      uint32_t fi = 0;
+      int32_t tk = 0;
+      int ni = 0, np = 0xFFFF, dp = 0, stt = 0;
+      if (keep) {
+        sc = P.score[i];
+        nu = P.num[i];
+        fi = P.first[i];
+        tk = P.tok[i];
+        dp = P.depth[i];
+        stt = P.state[i];
+        ni = P.aux[i];
+        if (i > 0) np = P.aux[P.par[i]];
+      }
+      __syncthreads();
+      if (keep) {
+        P.score[ni] = sc;
+        P.num[ni] = nu;
+        P.first[ni] = fi;
+        P.tok[ni] = tk;
+        P.par[ni] = static_cast<uint16_t>(np);
+        P.depth[ni] = static_cast<uint8_t>(dp);
+        P.state[ni] = static_cast<uint8_t>(stt);
+      }
+      __syncthreads();
+    }
+  }
+  if (lane == 0) P.m = static_cast<uint32_t>(kept);
+  __syncthreads();
+  return kept;
+}
+
+// Drafts the tree below u (child-list head u_head) and writes rows 1 .. n-1 of
+// it; returns n, or 0 if the candidates overflowed the pool (nothing written).
+__device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_head, int budget, int limit,
+                            double min_score, int32_t* __restrict__ tree_tokens, int32_t* __restrict__ tree_parent,
+                            int32_t* __restrict__ tree_depth) {
+  if (lane == 0) {
+    P.score[0] = 1.0;
+    P.first[0] = u_head;
+    P.par[0] = 0xFFFF;
+    P.depth[0] = 0;
+    P.state[0] = kOpen;
+    P.m = 1;
+  }
+  __syncthreads();
+  int M = 1;
+  for (;;) {
+    if (M > kPool / 2) M = compact(P, lane, M, budget);
+    // List the open entries, then drop those that can no longer be selected.
+    int n_open = 0;
+    for (int base = 0; base < M; base += SRT_WAVE) {
+      const int i = base + lane;
+      const bool open = i < M && P.state[i] == kOpen;
+      const uint64_t bal = __ballot(open);
+      if (open) P.list[n_open + rank_below(bal)] = static_cast<uint16_t>(i);
+      n_open += __popcll(bal);
+    }
+    if (n_open > 0 && M - 1 > budget) {
+      __syncthreads();
+      n_open = by_chunks(n_open, [&](auto rc) { return drop_listed<decltype(rc)::value>(P, lane, M, n_open, budget); });
+    }
+    if (n_open == 0) break;
+    __syncthreads();
+    // Walk their child lists, one list per lane: each step loads the next
+    // pointer, count, token and list head of a child together.
+    for (int j = lane; j < n_open; j += SRT_WAVE) {
+      const int i = P.list[j];
+      const int cd = P.depth[i] + 1;
+      const uint8_t cstate = cd >= limit ? kDone : kOpen;
+      uint32_t c = P.first[i];
+      unsigned long long total = 0;
+      while (c != kNone) {
+        const uint32_t nx = t.next[c];
+        const uint32_t cn = t.count[c];
+        const int32_t tk = static_cast<int32_t>(t.keys[c] & 0xFFFFFFFFull);
+        const uint32_t f = t.first[c];
+        const uint32_t slot = atomicAdd(&P.m, 1u);
+        if (slot >= static_cast<uint32_t>(kPool)) break;
+        P.num[slot] = cn;
+        P.tok[slot] = tk;
+        P.first[slot] = f;
+        P.par[slot] = static_cast<uint16_t>(i);
+        P.depth[slot] = static_cast<uint8_t>(cd);
+        P.state[slot] = f == kNone ? kDone : cstate;
+        total += cn;
+        c = nx;
+      }
+      P.num[i] = total;
+      P.state[i] = kDone;
+    }
+    __syncthreads();
+    const uint32_t m1 = P.m;
+    if (m1 > static_cast<uint32_t>(kPool)) return 0;
+    // Scores of the new entries: C(v), then the path product.
+    for (int i = M + lane; i < static_cast<int>(m1); i += SRT_WAVE) {
+      const int pa = P.par[i];
+      const double cv = static_cast<double>(static_cast<uint32_t>(P.num[i])) / static_cast<double>(P.num[pa]);
+      double sc = P.score[pa] * cv;
+      if (min_score > 0.0 && sc < min_score) {  // never selected, nor any descendant
+        sc = -1.0;
+        P.state[i] = kDropped;
+      }
+      P.score[i] = sc;
+    }
+    __syncthreads();
+    M = static_cast<int>(m1);
+  }
+
+  __syncthreads();
+  M = compact(P, lane, M, budget);
+
+  // Entries 1 .. M-1 listed by depth (counting sort).
+  P.dcount[lane] = 0;
+  __syncthreads();
+  for (int i = 1 + lane; i < M; i += SRT_WAVE) P.pos[i] = static_cast<uint16_t>(atomicAdd(&P.dcount[P.depth[i]], 1u));
+  __syncthreads();
+  const int cnt = static_cast<int>(P.dcount[lane]);  // lane = depth
+  int start = cnt;
+#pragma unroll
+  for (int off = 1; off < SRT_WAVE; off <<= 1) {
+    const int o = __shfl_up(start, off, SRT_WAVE);
+    if (lane >= off) start += o;
+  }
+  start -= cnt;
+  P.dstart[lane] = static_cast<uint32_t>(start);
+  __syncthreads();
+  for (int i = 1 + lane; i < M; i += SRT_WAVE) P.list[P.dstart[P.depth[i]] + P.pos[i]] = static_cast<uint16_t>(i);
+  const uint64_t used = __ballot(cnt > 0);
+  const int maxd = used ? 63 - __clzll(static_cast<long long>(used)) : 0;
+  if (lane == 0) P.aux[0] = 0;
+  __syncthreads();
+
+  // Rank of each token path among the paths of its depth, a depth at a time:
+  // it orders (parent's rank, token).  num holds the keys of one depth.
+  for (int d = 1; d <= maxd; ++d) {
+    const int n = __shfl(cnt, d, SRT_WAVE);
+    const int s0 = __shfl(start, d, SRT_WAVE);
+    for (int j = lane; j < n; j += SRT_WAVE) {
+      const int i = P.list[s0 + j];
+      P.num[s0 + j] = (static_cast<unsigned long long>(P.aux[P.par[i]]) << 32) | static_cast<uint32_t>(P.tok[i]);
+    }
+    __syncthreads();
+    for (int j = lane; j < n; j += SRT_WAVE) {
+      const unsigned long long k = P.num[s0 + j];
+      int r = 0;
+#pragma unroll 4
+      for (int w = 0; w < n; ++w) r += static_cast<int>(P.num[s0 + w] < k);
+      P.aux[P.list[s0 + j]] = static_cast<uint16_t>(r);
+    }
+    __syncthreads();
+  }
+
+  // Position in the total order: score descending, depth ascending, token
+  // path ascending (the tie key packs the last two, larger first).
+  for (int i = lane; i < M; i += SRT_WAVE)
+    P.num[i] = (static_cast<unsigned long long>(63 - P.depth[i]) << 16) | static_cast<uint32_t>(0xFFFF - P.aux[i]);
+  __syncthreads();
+  by_chunks(M, [&](auto rc) {
+    positions<decltype(rc)::value>(P, lane, M);
+    return 0;
+  });
+  __syncthreads();
+  for (int i = 1 + lane; i < M; i += SRT_WAVE) {
+    const int ps = P.pos[i];
+    if (ps < budget) {
+      const int pa = P.par[i];
+      tree_tokens[ps + 1] = P.tok[i];
+      tree_parent[ps + 1] = pa == 0 ? 0 : P.pos[pa] + 1;
+      tree_depth[ps + 1] = P.depth[i];
+    }
+  }
+  return 1 + min(budget, M - 1);
 }
 
 // Lane 0 walks up to kChildBuf list entries starting at sm.cursor.  For
@@ -258,7 +610,10 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
                                                    int32_t* __restrict__ tree_tokens, int32_t* __restrict__ tree_parent,
                                                    int32_t* __restrict__ tree_depth, int32_t* __restrict__ n_nodes,
                                                    int32_t* __restrict__ match_len) {
-  __shared__ Smem sm;
+  __shared__ union {
+    Smem seq;
+    Pool pool;
+  } shared;
   const TrieView t = trie_view_dev(ws);
   const int D = t.depth;
   const int b = blockIdx.x;
@@ -292,7 +647,32 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
     if (f < static_cast<double>(budget)) budget = static_cast<int>(f);
   }
   const int limit = qstar > 0 ? min(a.Dmax, D - qstar) : 0;
+  const bool chain = a.chain != 0;
+  const int64_t row = static_cast<int64_t>(b) * N;
 
+  if (!chain && qstar > 0 && budget > 0 && limit > 0) {
+    const int n = draft_levels(t, shared.pool, lane, u_head, budget, limit, a.min_score, tree_tokens + row,
+                               tree_parent + row, tree_depth + row);
+    if (n > 0) {
+      for (int i = n + lane; i < N; i += SRT_WAVE) {
+        tree_tokens[row + i] = -1;
+        tree_parent[row + i] = -1;
+        tree_depth[row + i] = -1;
+      }
+      if (lane == 0) {
+        tree_tokens[row] = root_tok;
+        tree_parent[row] = -1;
+        tree_depth[row] = 0;
+        n_nodes[b] = n;
+        match_len[b] = qstar;
+      }
+      return;
+    }
+    __syncthreads();  // the pool and the one-at-a-time state share memory
+  }
+
+  // One node at a time (chain drafts, and tree drafts that overflowed the pool).
+  Smem& sm = shared.seq;
   if (lane == 0) {
     sm.sel_first[0] = qstar > 0 ? u_head : kNone;
     sm.sel_tok[0] = root_tok;
@@ -303,7 +683,6 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
   }
   __syncthreads();
   int nsel = 1, fsize = 0;
-  const bool chain = a.chain != 0;
   if (qstar > 0 && budget > 0 && limit > 0) expand(t, sm, 0, lane, fsize, chain);
 
   while (nsel - 1 < budget && fsize > 0) {
@@ -353,7 +732,6 @@ __global__ __launch_bounds__(64) void draft_kernel(const void* ws, const int32_t
     if (depth < limit) expand(t, sm, nsel - 1, lane, fsize, chain);
   }
 
-  const int64_t row = static_cast<int64_t>(b) * N;
   for (int i = lane; i < N; i += SRT_WAVE) {
     const bool in = i < nsel;
     tree_tokens[row + i] = in ? sm.sel_tok[i] : -1;

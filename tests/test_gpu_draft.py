@@ -1,7 +1,9 @@
 """GPU parity of srt_draft against the oracle draft, bit-exact: the tiny
 configuration, random small-vocabulary caches full of score ties, budget and
-depth variants, score thresholds and chain drafts, fallbacks, and a frontier
-overflow (also with chain drafts over a 1500-child list)."""
+depth variants, score thresholds and chain drafts, fallbacks, a candidate pool
+pruned while more than half full, and a 1500-child list that overflows the
+pool (the one-at-a-time path then runs, its frontier evicting; also with chain
+drafts)."""
 import random
 
 import numpy as np
@@ -83,6 +85,30 @@ def test_frontier_overflow_and_long_child_lists():
         say(f"draft: long child list tau={tau} chain={chain}")
         tree = run_draft(c, [0], [[7]], [5], 1, 256, 2, 0.0, tau, chain)
         assert_tree_equal(tree, 0, DR.draft(trie, [7], 5, 1, 256, 2, 0.0, tau, chain))
+
+
+def test_pool_over_half_full():
+    # u = (7) has 8 children with 70 children each (560 grandchildren whose
+    # counts repeat with period 13, so scores tie in groups); each grandchild
+    # has up to 3 children.  Drafting 63 nodes first discovers all 560
+    # grandchildren, so the candidate pool passes 512 entries and is pruned to
+    # what can still be selected before the next level is walked.
+    rng = np.random.default_rng(5)
+    streams = []
+    for a in range(8):
+        for b in range(70):
+            for _ in range(1 + (a * 70 + b) % 13):
+                streams.append(np.array([7, 100 + a, 200 + b, 300 + int(rng.integers(0, 3))]))
+    D = 6
+    c = Caches.create(1, len(streams) + 1, D, 200000)
+    c.insert([0] * len(streams), c.new_streams(len(streams)), streams)
+    trie = TR.DictTrie(TR.substring_counts(streams, D), D)
+    for N, Dmax, alpha, tau in [(64, 3, 0.0, 0.0), (64, 2, 0.0, 0.0), (256, 3, 0.0, 0.0), (64, 3, 0.0, 1e-3),
+                                (200, 3, 0.0, 0.0)]:
+        say(f"draft: pool over half full N={N} Dmax={Dmax} tau={tau}")
+        tree = run_draft(c, [0], [[7]], [5], 1, N, Dmax, alpha, tau)
+        assert_tree_equal(tree, 0, DR.draft(trie, [7], 5, 1, N, Dmax, alpha, tau))
+        assert int(tree["n_nodes"][0]) > 1
 
 
 @pytest.mark.parametrize("tau,chain", [(0.0, True), (0.02, False)])
