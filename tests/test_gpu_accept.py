@@ -1,7 +1,9 @@
 """GPU parity of srt_accept against the oracle walk, bit-exact: greedy and
 Gumbel sampling, temperatures, ties, vocabularies with and without 16-byte
 alignment, depth caps, long accepted paths; large vocabularies split over
-up to 32 cooperating workgroups per sequence, with ties across slices."""
+up to 32 cooperating workgroups per sequence, with ties across slices;
+batches of 70-300 sequences with deep walks, and 4000 sequences that all
+walk at least three steps deep."""
 import random
 
 import numpy as np
@@ -87,3 +89,87 @@ def test_depth_cap_and_chain():
     want = oracle_accept_rows(logits, None, 1.0, tree, [0], Dmax)
     assert_accept_equal(got, 0, want[0], Dmax)
     assert int(got["n_accepted"][0]) == Dmax
+
+
+def deep_trees(rng, B, N, Dmax, V):
+    """Trees that mostly extend their newest node (paths of depth up to Dmax)."""
+    tt = np.full((B, N), -1, np.int32)
+    tp = np.full((B, N), -1, np.int32)
+    td = np.full((B, N), -1, np.int32)
+    nn = np.zeros(B, np.int32)
+    for b in range(B):
+        n = rng.randrange(1, N + 1)
+        tt[b, 0], td[b, 0] = rng.randrange(V), 0
+        used = set()
+        k = 1
+        while k < n:
+            p = k - 1 if rng.random() < 0.75 else rng.randrange(k)
+            if td[b, p] >= Dmax:
+                p = rng.randrange(k)
+                if td[b, p] >= Dmax:
+                    continue
+            x = rng.randrange(V)
+            if (p, x) in used:
+                continue
+            used.add((p, x))
+            tt[b, k], tp[b, k], td[b, k] = x, p, td[b, p] + 1
+            k += 1
+        nn[b] = k
+    return {"tree_tokens": tt, "tree_parent": tp, "tree_depth": td, "n_nodes": nn}
+
+
+@pytest.mark.parametrize("B,V,sampled,ties", [(100, 152064, True, False), (100, 152064, False, True),
+                                              (300, 1024, True, False), (70, 50001, False, False)])
+def test_walk_exact_large_batch(B, V, sampled, ties):
+    # a node's last child gets +30 with p = 0.9, so most walks go deep and the
+    # late levels run with few walkers left
+    rng = random.Random(B * 13 + V)
+    N, Dmax = 32, 12
+    say(f"accept: B={B} V={V} sampled={sampled} ties={ties}")
+    tree = deep_trees(rng, B, N, Dmax, V)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(B + V)
+    logits = torch.randn((B, N, V), generator=g, device="cuda") * 2.0
+    if ties:  # integer logits: row maxima repeat, also across the slices of a row
+        logits = torch.round(logits)
+    bi, ui, ti = [], [], []
+    for b in range(B):
+        for c in range(1, int(tree["n_nodes"][b])):
+            if rng.random() < 0.9:  # later children overwrite: the node's last child wins
+                bi.append(b), ui.append(int(tree["tree_parent"][b, c])), ti.append(int(tree["tree_tokens"][b, c]))
+    logits[torch.tensor(bi), torch.tensor(ui), torch.tensor(ti)] = 30.0
+    gumbel = None
+    if sampled:
+        gumbel = -torch.log(-torch.log(torch.rand((B, Dmax + 1, V), generator=g, device="cuda")
+                                       .clamp_(1e-20, 1.0 - 1e-7)))
+    got = run(tree, logits, gumbel, 1.0, Dmax)
+    want = oracle_accept_rows(logits, gumbel, 1.0, tree, range(B), Dmax)
+    for b in range(B):
+        assert_accept_equal(got, b, want[b], Dmax)
+    assert (got["n_accepted"] >= 4).sum() >= 5  # deep walks
+
+
+def test_many_deep_walks():
+    # 4000 chains of 6 nodes whose logits lead down each chain: all 4000 walks
+    # reach the fourth step (the level lists hold every sequence)
+    B, N, V, Dmax = 4000, 6, 16, 5
+    tt = np.tile(np.array([3, 5, 7, 9, 11, 13], np.int32), (B, 1))
+    tp = np.tile(np.arange(-1, N - 1, dtype=np.int32), (B, 1))
+    nn = np.full(B, N, np.int32)
+    rng = np.random.default_rng(3)
+    logits = rng.normal(0.0, 1.0, (B, N, V)).astype(np.float32)
+    stop = rng.integers(3, N, B)  # the walk of b leaves its chain at node stop[b]
+    for b in range(B):
+        for u in range(N - 1):
+            if u != stop[b]:
+                logits[b, u, tt[b, u + 1]] = 10.0
+    tree = {"tree_tokens": tt, "tree_parent": tp, "n_nodes": nn}
+    logits = torch.from_numpy(logits).cuda()
+    gumbel = torch.from_numpy(rng.gumbel(size=(B, Dmax + 1, V)).astype(np.float32) * 0.1).cuda()
+    for g in (None, gumbel):
+        say(f"accept: {B} walks past the third step, sampled={g is not None}")
+        got = run(tree, logits, g, 1.0, Dmax)
+        want = oracle_accept_rows(logits, g, 1.0, tree, range(B), Dmax)
+        for b in range(B):
+            assert_accept_equal(got, b, want[b], Dmax)
+        assert (got["n_accepted"] >= 3).all()
