@@ -146,12 +146,12 @@ struct Pool {
   uint32_t first[kPool];          // child-list head
   int32_t tok[kPool];
   uint16_t par[kPool];
-  uint16_t aux[kPool];            // compaction map, then rank of the token path among its depth
-  uint16_t pos[kPool];            // slot within its depth, then position in the selection order
+  uint16_t aux[kPool];            // compaction map, rank of the token path among its depth, position
+  uint16_t pos[kPool];            // entries scoring strictly higher (set by compaction)
   uint16_t list[kPool];           // entries to expand; then all entries, by depth
   uint8_t depth[kPool];
   uint8_t state[kPool];
-  uint32_t dcount[64];            // entries per depth
+  uint32_t dcount[64];            // entries per depth (then per depth slot)
   uint32_t dstart[64];            // first list slot of each depth
   uint32_t m;                     // entries in use; appends reserve slots here
 };
@@ -176,18 +176,15 @@ __device__ inline auto by_chunks(int n, F f) {
   return f(std::integral_constant<int, kPool / SRT_WAVE>{});
 }
 
-// c[r] += the number of entries w in 1 .. M-1 ranking strictly above key r:
-// a larger score or, with kTies, an equal score and a larger tie key (num).
+// c[r] += the number of entries w in 1 .. M-1 scoring strictly above key r.
 // Each entry is read from LDS once and compared with all R keys held here.
-template <int R, bool kTies>
-__device__ inline void count_above(const Pool& P, int M, const int64_t (&ks)[R], const uint32_t (&kt)[R],
-                                   int (&c)[R]) {
+template <int R>
+__device__ inline void count_above(const Pool& P, int M, const int64_t (&ks)[R], int (&c)[R]) {
 #pragma unroll 4
   for (int w = 1; w < M; ++w) {
     const int64_t sw = score_key(P.score[w]);
-    const uint32_t tw = kTies ? static_cast<uint32_t>(P.num[w]) : 0u;
 #pragma unroll
-    for (int r = 0; r < R; ++r) c[r] += static_cast<int>((sw > ks[r]) | (kTies & (sw == ks[r]) & (tw > kt[r])));
+    for (int r = 0; r < R; ++r) c[r] += static_cast<int>(sw > ks[r]);
   }
 }
 
@@ -197,16 +194,14 @@ template <int R>
 __device__ int drop_listed(Pool& P, int lane, int M, int n, int budget) {
   int idx[R], c[R];
   int64_t ks[R];
-  uint32_t kt[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int j = lane + SRT_WAVE * r;
     idx[r] = j < n ? P.list[j] : -1;
     ks[r] = idx[r] >= 0 ? score_key(P.score[idx[r]]) : kNoKey;
-    kt[r] = 0;
     c[r] = 0;
   }
-  count_above<R, false>(P, M, ks, kt, c);
+  count_above<R>(P, M, ks, c);
   __syncthreads();  // every lane has read the list
   int kept = 0;
 #pragma unroll
@@ -222,21 +217,21 @@ __device__ int drop_listed(Pool& P, int lane, int M, int n, int budget) {
 
 // Marks for keeping entry 0 and every entry that can still be selected (not
 // dropped, fewer than `budget` entries of strictly larger score), drops the
-// rest, and writes each kept entry's new index to aux; returns the count.
+// rest, writes each kept entry's new index to aux and its count of entries
+// scoring strictly higher to pos; returns the number kept.  Every entry
+// scoring above a kept one is kept too, so the count holds after compaction.
 template <int R>
 __device__ int keep_marks(Pool& P, int lane, int M, int budget) {
   int c[R];
   int64_t ks[R];
-  uint32_t kt[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int i = lane + SRT_WAVE * r;
     const bool live = i >= 1 && i < M && P.state[i] != kDropped;
     ks[r] = live ? score_key(P.score[i]) : kNoKey;
-    kt[r] = 0;
     c[r] = 0;
   }
-  count_above<R, false>(P, M, ks, kt, c);
+  count_above<R>(P, M, ks, c);
   int kept = 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -244,33 +239,13 @@ __device__ int keep_marks(Pool& P, int lane, int M, int budget) {
     const bool keep = i == 0 || (i < M && ks[r] != kNoKey && c[r] < budget);
     if (i < M && !keep) P.state[i] = kDropped;
     const uint64_t bal = __ballot(keep);
-    if (keep) P.aux[i] = static_cast<uint16_t>(kept + rank_below(bal));
+    if (keep) {
+      P.aux[i] = static_cast<uint16_t>(kept + rank_below(bal));
+      P.pos[i] = static_cast<uint16_t>(c[r]);
+    }
     kept += __popcll(bal);
   }
   return kept;
-}
-
-// Position of every entry 1 .. M-1 in the selection order, from its score and
-// the tie key in num.
-template <int R>
-__device__ void positions(Pool& P, int lane, int M) {
-  int c[R];
-  int64_t ks[R];
-  uint32_t kt[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int i = lane + SRT_WAVE * r;
-    const bool v = i >= 1 && i < M;
-    ks[r] = v ? score_key(P.score[i]) : kNoKey;
-    kt[r] = v ? static_cast<uint32_t>(P.num[i]) : ~0u;
-    c[r] = 0;
-  }
-  count_above<R, true>(P, M, ks, kt, c);
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int i = lane + SRT_WAVE * r;
-    if (i >= 1 && i < M) P.pos[i] = static_cast<uint16_t>(c[r]);
-  }
 }
 
 // Keeps entry 0 and every entry that can still be selected, moved down in
@@ -289,8 +264,9 @@ __device__ __forceinline__ int compact(Pool& P, int lane, int M, int budget) {
       unsigned long long nu = 0;
       uint32_t fi = 0;
       int32_t tk = 0;
-      int ni = 0, np = 0xFFFF, dp = 0, stt = 0;
+      int ni = 0, np = 0xFFFF, dp = 0, stt = 0, above = 0;
       if (keep) {
+        above = P.pos[i];
         sc = P.score[i];
         nu = P.num[i];
         fi = P.first[i];
@@ -309,6 +285,7 @@ __device__ __forceinline__ int compact(Pool& P, int lane, int M, int budget) {
         P.par[ni] = static_cast<uint16_t>(np);
         P.depth[ni] = static_cast<uint8_t>(dp);
         P.state[ni] = static_cast<uint8_t>(stt);
+        P.pos[ni] = static_cast<uint16_t>(above);
       }
       __syncthreads();
     }
@@ -401,7 +378,7 @@ __device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_hea
   // Entries 1 .. M-1 listed by depth (counting sort).
   P.dcount[lane] = 0;
   __syncthreads();
-  for (int i = 1 + lane; i < M; i += SRT_WAVE) P.pos[i] = static_cast<uint16_t>(atomicAdd(&P.dcount[P.depth[i]], 1u));
+  for (int i = 1 + lane; i < M; i += SRT_WAVE) P.aux[i] = static_cast<uint16_t>(atomicAdd(&P.dcount[P.depth[i]], 1u));
   __syncthreads();
   const int cnt = static_cast<int>(P.dcount[lane]);  // lane = depth
   int start = cnt;
@@ -413,9 +390,10 @@ __device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_hea
   start -= cnt;
   P.dstart[lane] = static_cast<uint32_t>(start);
   __syncthreads();
-  for (int i = 1 + lane; i < M; i += SRT_WAVE) P.list[P.dstart[P.depth[i]] + P.pos[i]] = static_cast<uint16_t>(i);
+  for (int i = 1 + lane; i < M; i += SRT_WAVE) P.list[P.dstart[P.depth[i]] + P.aux[i]] = static_cast<uint16_t>(i);
   const uint64_t used = __ballot(cnt > 0);
   const int maxd = used ? 63 - __clzll(static_cast<long long>(used)) : 0;
+  __syncthreads();
   if (lane == 0) P.aux[0] = 0;
   __syncthreads();
 
@@ -439,22 +417,36 @@ __device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_hea
     __syncthreads();
   }
 
-  // Position in the total order: score descending, depth ascending, token
-  // path ascending (the tie key packs the last two, larger first).
-  for (int i = lane; i < M; i += SRT_WAVE)
-    P.num[i] = (static_cast<unsigned long long>(63 - P.depth[i]) << 16) | static_cast<uint32_t>(0xFFFF - P.aux[i]);
-  __syncthreads();
-  by_chunks(M, [&](auto rc) {
-    positions<decltype(rc)::value>(P, lane, M);
-    return 0;
-  });
+  // Position in the total order (score descending, depth ascending, token
+  // path ascending).  Entries of equal score share their count of entries
+  // scoring higher, which is where their group starts; within a group they
+  // rank by the tie key (depth and path rank packed, larger first).  The keys
+  // are gathered in group order by a counting sort on that start (into num;
+  // the walks and their counts are done with it).
+  for (int i = lane; i < M; i += SRT_WAVE) P.first[i] = 0;  // group sizes
   __syncthreads();
   for (int i = 1 + lane; i < M; i += SRT_WAVE) {
-    const int ps = P.pos[i];
+    const int g0 = P.pos[i];
+    P.num[g0 + atomicAdd(&P.first[g0], 1u)] =
+        (static_cast<unsigned long long>(63 - P.depth[i]) << 16) | static_cast<uint32_t>(0xFFFF - P.aux[i]);
+  }
+  __syncthreads();
+  for (int i = 1 + lane; i < M; i += SRT_WAVE) {
+    const int g0 = P.pos[i];
+    const int g = static_cast<int>(P.first[g0]);
+    const unsigned long long k =
+        (static_cast<unsigned long long>(63 - P.depth[i]) << 16) | static_cast<uint32_t>(0xFFFF - P.aux[i]);
+    int r = 0;
+    for (int j = 0; j < g; ++j) r += static_cast<int>(P.num[g0 + j] > k);
+    P.aux[i] = static_cast<uint16_t>(g0 + r);
+  }
+  __syncthreads();
+  for (int i = 1 + lane; i < M; i += SRT_WAVE) {
+    const int ps = P.aux[i];
     if (ps < budget) {
       const int pa = P.par[i];
       tree_tokens[ps + 1] = P.tok[i];
-      tree_parent[ps + 1] = pa == 0 ? 0 : P.pos[pa] + 1;
+      tree_parent[ps + 1] = pa == 0 ? 0 : P.aux[pa] + 1;
       tree_depth[ps + 1] = P.depth[i];
     }
   }
