@@ -188,28 +188,42 @@ __device__ inline void count_above(const Pool& P, int M, const int64_t (&ks)[R],
   }
 }
 
-// Drops the n listed open entries that have `budget` or more entries of
-// strictly larger score, and compacts the list; returns its new length.
+// The `budget`-th largest score key among entries 1 .. M-1 (0 if fewer than
+// `budget` entries score above 0; entries below the score threshold never
+// count), found bit by bit from the top with wave ballots.  An entry has fewer
+// than `budget` entries of strictly larger score exactly when its key is at
+// least this value.
 template <int R>
-__device__ int drop_listed(Pool& P, int lane, int M, int n, int budget) {
-  int idx[R], c[R];
-  int64_t ks[R];
+__device__ int64_t kth_score_key(const Pool& P, int lane, int M, int budget) {
+  int64_t k[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int j = lane + SRT_WAVE * r;
-    idx[r] = j < n ? P.list[j] : -1;
-    ks[r] = idx[r] >= 0 ? score_key(P.score[idx[r]]) : kNoKey;
-    c[r] = 0;
+    const int i = lane + SRT_WAVE * r;
+    k[r] = i >= 1 && i < M ? score_key(P.score[i]) : -1;
   }
-  count_above<R>(P, M, ks, c);
-  __syncthreads();  // every lane has read the list
-  int kept = 0;
+  int64_t t = 0;
+  for (int bit = 62; bit >= 0; --bit) {
+    const int64_t c = t | (int64_t{1} << bit);
+    int n = 0;
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const bool keep = idx[r] >= 0 && c[r] < budget;
-    const uint64_t bal = __ballot(keep);
-    if (keep) P.list[kept + rank_below(bal)] = static_cast<uint16_t>(idx[r]);
-    else if (idx[r] >= 0) P.state[idx[r]] = kDropped;
+    for (int r = 0; r < R; ++r) n += __popcll(__ballot(k[r] >= c));
+    if (n >= budget) t = c;
+  }
+  return t;
+}
+
+// Drops the n listed open entries whose score key is below t (they have
+// `budget` or more entries of strictly larger score) and compacts the list in
+// place; returns its new length.
+__device__ int drop_below(Pool& P, int lane, int n, int64_t t) {
+  int kept = 0;
+  for (int base = 0; base < n; base += SRT_WAVE) {
+    const int j = base + lane;
+    const int i = j < n ? P.list[j] : -1;
+    const bool keep = i >= 0 && score_key(P.score[i]) >= t;
+    const uint64_t bal = __ballot(keep);  // every lane has read its entry
+    if (keep) P.list[kept + rank_below(bal)] = static_cast<uint16_t>(i);
+    else if (i >= 0) P.state[i] = kDropped;
     kept += __popcll(bal);
   }
   return kept;
@@ -323,7 +337,8 @@ __device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_hea
     }
     if (n_open > 0 && M - 1 > budget) {
       __syncthreads();
-      n_open = by_chunks(n_open, [&](auto rc) { return drop_listed<decltype(rc)::value>(P, lane, M, n_open, budget); });
+      const int64_t t = by_chunks(M, [&](auto rc) { return kth_score_key<decltype(rc)::value>(P, lane, M, budget); });
+      n_open = drop_below(P, lane, n_open, t);
     }
     if (n_open == 0) break;
     __syncthreads();
