@@ -21,10 +21,15 @@
 //     the arg-max with the lowest index (+0 and -0 compare equal, as fp32
 //     comparisons do).  Blocks map onto the rows that exist at the level,
 //     working blocks first in dispatch order.
-//   * A walk kernel (one wave per walker) takes the largest candidate of its
-//     row, looks for the child that carries the token, writes the step's
-//     output and, if it descends, appends the sequence to the next level's
-//     list.
+//   * The step's decision is folded into the next level's kernel: every
+//     block of a walker first takes the largest candidate of the walker's
+//     previous row, looks for the child that carries the token (all blocks
+//     of the walker reach the same answer), and one of them writes the
+//     step's output and, if it descends, appends the sequence to the next
+//     level's list; then each block reads its chunk of the child's row.  A
+//     last walk kernel decides the final level.  Candidates and current
+//     nodes alternate between two buffers by level parity, so no launch
+//     reads a buffer it writes.
 // x = fl(fl(l * inv_T) + g) is evaluated with explicitly rounded multiply
 // and add (no FMA), matching the fp32 reference bit for bit.
 #include <algorithm>
@@ -58,8 +63,8 @@ struct AcceptArgs {
   int32_t* n_emitted;
   int32_t* n_act;            // [kMaxLevels + 1] sequences walking at each level
   int32_t* act;              // [2, B] those sequences, by level parity
-  int32_t* cur;              // [B] node each sequence stands on
-  unsigned long long* cand;  // [B, kMaxChunks] packed candidates of the level
+  int32_t* cur;              // [2, B] node each sequence stands on, by level parity
+  unsigned long long* cand;  // [2, B, kMaxChunks] packed candidates of a level, by parity
   int B, N, V, Dmax, chunk, n_chunks;
   int vec;                   // rows can be read as float4
   float invT;
@@ -75,8 +80,8 @@ inline ScratchLayout scratch_layout(int64_t B) {
   ScratchLayout s;
   s.off_act = up(sizeof(int32_t) * (kMaxLevels + 1));
   s.off_cur = s.off_act + up(sizeof(int32_t) * 2 * static_cast<size_t>(B));
-  s.off_cand = s.off_cur + up(sizeof(int32_t) * static_cast<size_t>(B));
-  s.total = s.off_cand + up(sizeof(unsigned long long) * static_cast<size_t>(B) * kMaxChunks);
+  s.off_cand = s.off_cur + up(sizeof(int32_t) * 2 * static_cast<size_t>(B));
+  s.total = s.off_cand + up(sizeof(unsigned long long) * 2 * static_cast<size_t>(B) * kMaxChunks);
   return s;
 }
 
@@ -178,62 +183,98 @@ __global__ __launch_bounds__(256) void accept_init_kernel(AcceptArgs a) {
     a.out_nodes[row + k] = -1;
   }
   a.act[b] = b;
-  a.cur[b] = 0;
+  a.cur[b] = 0;  // level 0, parity 0
 }
 
-// One chunk of the visited row of one walker at this level.
-template <bool kNoise>
-__global__ __launch_bounds__(kThreads) void accept_level_kernel(AcceptArgs a, int level) {
-  const int g = blockIdx.x;
-  const int slot = g / a.n_chunks, c = g - slot * a.n_chunks;
-  if (slot >= a.n_act[level]) return;
-  const int b = min(max(a.act[(level & 1) * a.B + slot], 0), a.B - 1);
-  const int u = min(max(a.cur[b], 0), a.N - 1);
-  const float* row = a.logits + (static_cast<int64_t>(b) * a.N + u) * a.V;
-  const float* noise = kNoise ? a.gumbel + (static_cast<int64_t>(b) * (a.Dmax + 1) + level) * a.V : nullptr;
-  const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
-  const Best best = chunk_argmax<kNoise>(a, row, noise, lo, hi);
-  if (threadIdx.x == 0) a.cand[static_cast<int64_t>(slot) * kMaxChunks + c] = pack_key(best.v, best.i);
-}
+// The decision of step `level` for sequence b standing on node u, from the
+// candidates of its row, in one wave: the token, and the child that carries
+// it (-1 if none or if the walk is at its depth cap).
+struct Step {
+  int tok, child;
+};
 
-// One wave per walker: the step's token, then descend or stop.
-__global__ __launch_bounds__(kWalkWaves * SRT_WAVE) void accept_walk_kernel(AcceptArgs a, int level) {
-  const int lane = threadIdx.x % SRT_WAVE;
-  const int slot = blockIdx.x * kWalkWaves + threadIdx.x / SRT_WAVE;
-  if (slot >= a.n_act[level]) return;
-  unsigned long long best = lane < a.n_chunks ? a.cand[static_cast<int64_t>(slot) * kMaxChunks + lane] : 0ull;
+__device__ inline Step decide(const AcceptArgs& a, int b, int u, int level, int lane) {
+  const unsigned long long* cand = a.cand + (static_cast<int64_t>(level & 1) * a.B + b) * kMaxChunks;
+  unsigned long long best = lane < a.n_chunks ? cand[lane] : 0ull;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const unsigned long long o = shfl_xor_u64(best, off);
     best = o > best ? o : best;
   }
-  const int tok = key_token(best);
-  const int b = min(max(a.act[(level & 1) * a.B + slot], 0), a.B - 1);
-  const int u = a.cur[b];
+  Step st{key_token(best), -1};
   const int n = min(max(a.n_nodes[b], 1), a.N);
   const int64_t tr = static_cast<int64_t>(b) * a.N;
-  int child = -1;
   if (level < a.Dmax) {
-    for (int c0 = u + 1; c0 < n && child < 0; c0 += SRT_WAVE) {
+    for (int c0 = u + 1; c0 < n && st.child < 0; c0 += SRT_WAVE) {
       const int cc = c0 + lane;
-      const bool hit = cc < n && a.tree_parent[tr + cc] == u && a.tree_tokens[tr + cc] == tok;
+      const bool hit = cc < n && a.tree_parent[tr + cc] == u && a.tree_tokens[tr + cc] == st.tok;
       const unsigned long long m = __ballot(hit);
-      if (m) child = c0 + __ffsll(static_cast<long long>(m)) - 1;
+      if (m) st.child = c0 + __ffsll(static_cast<long long>(m)) - 1;
     }
   }
-  if (lane == 0) {
-    const int64_t orow = static_cast<int64_t>(b) * (a.Dmax + 1);
-    a.out_tokens[orow + level] = tok;
-    if (child >= 0) {
-      a.out_nodes[orow + level] = child;
-      a.cur[b] = child;
-      const int pos = atomicAdd(&a.n_act[level + 1], 1);
-      a.act[((level + 1) & 1) * a.B + pos] = b;
-    } else {
-      a.n_accepted[b] = level;
-      if (a.n_emitted) a.n_emitted[b] = level + 1;
-    }
+  return st;
+}
+
+// Records step `level` of sequence b (one thread): the token, then descend
+// (next node, next level's list) or stop.
+__device__ inline void record(const AcceptArgs& a, int b, int level, const Step& st) {
+  const int64_t orow = static_cast<int64_t>(b) * (a.Dmax + 1);
+  a.out_tokens[orow + level] = st.tok;
+  if (st.child >= 0) {
+    a.out_nodes[orow + level] = st.child;
+    a.cur[((level + 1) & 1) * a.B + b] = st.child;
+    const int pos = atomicAdd(&a.n_act[level + 1], 1);
+    a.act[((level + 1) & 1) * a.B + pos] = b;
+  } else {
+    a.n_accepted[b] = level;
+    if (a.n_emitted) a.n_emitted[b] = level + 1;
   }
+}
+
+// One chunk of the visited row of one walker at this level.  For level > 0
+// the walker is one of those of the previous level, and the block first
+// takes that level's step (block 0 of the walker records it).
+template <bool kNoise>
+__global__ __launch_bounds__(kThreads) void accept_level_kernel(AcceptArgs a, int level) {
+  const int g = blockIdx.x;
+  const int slot = g / a.n_chunks, c = g - slot * a.n_chunks;
+  const int lv = level > 0 ? level - 1 : 0;  // the list the walker comes from
+  if (slot >= a.n_act[lv]) return;
+  const int b = min(max(a.act[(lv & 1) * a.B + slot], 0), a.B - 1);
+  int u;
+  if (level == 0) {
+    u = 0;
+  } else {
+    __shared__ int s_child;
+    if (threadIdx.x < SRT_WAVE) {
+      const int prev = min(max(a.cur[(lv & 1) * a.B + b], 0), a.N - 1);
+      const Step st = decide(a, b, prev, lv, threadIdx.x);
+      if (threadIdx.x == 0) {
+        if (c == 0) record(a, b, lv, st);
+        s_child = st.child;
+      }
+    }
+    __syncthreads();
+    u = s_child;
+    if (u < 0) return;
+  }
+  const float* row = a.logits + (static_cast<int64_t>(b) * a.N + u) * a.V;
+  const float* noise = kNoise ? a.gumbel + (static_cast<int64_t>(b) * (a.Dmax + 1) + level) * a.V : nullptr;
+  const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
+  const Best best = chunk_argmax<kNoise>(a, row, noise, lo, hi);
+  if (threadIdx.x == 0)
+    a.cand[(static_cast<int64_t>(level & 1) * a.B + b) * kMaxChunks + c] = pack_key(best.v, best.i);
+}
+
+// The step of the last level (Dmax), one wave per walker.
+__global__ __launch_bounds__(kWalkWaves * SRT_WAVE) void accept_walk_kernel(AcceptArgs a, int level) {
+  const int lane = threadIdx.x % SRT_WAVE;
+  const int slot = blockIdx.x * kWalkWaves + threadIdx.x / SRT_WAVE;
+  if (slot >= a.n_act[level]) return;
+  const int b = min(max(a.act[(level & 1) * a.B + slot], 0), a.B - 1);
+  const int u = min(max(a.cur[(level & 1) * a.B + b], 0), a.N - 1);
+  const Step st = decide(a, b, u, level, lane);
+  if (lane == 0) record(a, b, level, st);
 }
 
 }  // namespace
@@ -294,8 +335,9 @@ extern "C" int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const f
     else
       accept_level_kernel<false><<<static_cast<unsigned>(grid), kThreads, 0, s>>>(a, level);
     st = launch_status();
-    if (st != SRT_OK) break;
-    accept_walk_kernel<<<walk_grid, kWalkWaves * SRT_WAVE, 0, s>>>(a, level);
+  }
+  if (st == SRT_OK) {
+    accept_walk_kernel<<<walk_grid, kWalkWaves * SRT_WAVE, 0, s>>>(a, Dmax);
     st = launch_status();
   }
   return st;
