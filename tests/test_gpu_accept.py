@@ -173,3 +173,29 @@ def test_many_deep_walks():
         for b in range(B):
             assert_accept_equal(got, b, want[b], Dmax)
         assert (got["n_accepted"] >= 3).all()
+
+
+@pytest.mark.parametrize("Dmax,sampled", [(63, False), (63, True), (62, True)])
+def test_deepest_walk(Dmax, sampled):
+    # a 64-node chain whose logits lead down it: the walk takes every level up
+    # to the depth cap (all 64 levels when Dmax = 63), the level buffers
+    # alternating between their two halves throughout
+    B, N, V = 3, 64, 4096
+    tt = np.zeros((B, N), np.int32)
+    for b in range(B):
+        tt[b] = (np.arange(N) * 37 + 11 * b) % V
+    tp = np.tile(np.arange(-1, N - 1, dtype=np.int32), (B, 1))
+    g = torch.Generator(device="cuda")
+    g.manual_seed(Dmax)
+    logits = torch.randn((B, N, V), generator=g, device="cuda")
+    for b in range(B):
+        for u in range(N - 1):
+            logits[b, u, int(tt[b, u + 1])] = 50.0
+    gumbel = torch.rand((B, Dmax + 1, V), generator=g, device="cuda") if sampled else None
+    tree = {"tree_tokens": tt, "tree_parent": tp, "n_nodes": np.full(B, N, np.int32)}
+    say(f"accept: deepest walk Dmax={Dmax} sampled={sampled}")
+    got = run(tree, logits, gumbel, 1.0, Dmax)
+    want = oracle_accept_rows(logits, gumbel, 1.0, tree, range(B), Dmax)
+    for b in range(B):
+        assert_accept_equal(got, b, want[b], Dmax)
+    assert (got["n_accepted"] == min(Dmax, N - 1)).all()
