@@ -1,7 +1,7 @@
 """GPU parity of srt_accept against the oracle walk, bit-exact: greedy and
 Gumbel sampling, temperatures, ties, vocabularies with and without 16-byte
 alignment, depth caps, long accepted paths; large vocabularies split over
-up to 32 cooperating workgroups per sequence, with ties across slices;
+up to 32 workgroups per row (chunks), with ties across chunks;
 batches of 70-300 sequences with deep walks, and 4000 sequences that all
 walk at least three steps deep."""
 import random
