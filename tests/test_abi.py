@@ -111,6 +111,9 @@ def test_host_validation_before_any_hip_call():
     assert L.srt_draft(ctypes.c_void_p(256), 2, *[None] * 3, ctypes.byref(p), *[None] * 6) == S.SRT_ERR_INVALID
     args = [4, 8, 4, 1, 96, 16, 40, 100] + [ctypes.c_void_p(256)] * 7 + [0.125, ctypes.c_void_p(256), None, 0, None]
     assert L.srt_tree_attn(*args) == S.SRT_ERR_UNSUPPORTED           # d = 96
+    for bad_page in (8, 24, 48):
+        a2 = list(args); a2[4] = 64; a2[5] = bad_page
+        assert L.srt_tree_attn(*a2) == S.SRT_ERR_UNSUPPORTED         # page not a power of two >= 16
     args[4] = 64; args[2] = 5; args[3] = 2
     assert L.srt_tree_attn(*args) == S.SRT_ERR_INVALID               # Hq % Hkv
     args[2] = 4; args[3] = 1; args[1] = 300

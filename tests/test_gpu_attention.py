@@ -2,7 +2,7 @@
 |gpu - ref| <= 1e-2 + 2e-2 |ref| over every output row, for the tiny
 configuration and for shapes that span several key tiles, ragged tails,
 split contexts (with the combine pass), both head sizes, GQA ratios 1-7,
-256-node trees, one-node trees and empty contexts."""
+256-node trees, one-node trees, empty contexts and pages of 16-256 tokens."""
 import math
 import random
 
@@ -105,10 +105,10 @@ def test_split_contexts_mid_size_splits(B, split):
     c.check(c.run(), seqs=list(range(len(base))))
 
 
-@pytest.mark.parametrize("page,d", [(32, 128), (64, 128), (64, 64)])
+@pytest.mark.parametrize("page,d", [(32, 128), (64, 128), (64, 64), (128, 128), (256, 64)])
 def test_larger_pages(page, d):
-    # pages of 32 and 64 tokens: a 64-key tile spans two or one page, ragged
-    # tails and split contexts included
+    # pages of 32 to 256 tokens: a 64-key tile spans two pages or lies inside
+    # one, ragged tails and split contexts included
     say(f"attn: page {page}, d={d}")
     ctx = [0, 31, 32, 33, 63, 64, 65, 1000, 9000, 4097]
     c = Case(43 + page, len(ctx), 16, 8, 2, d, ctx, page=page)
