@@ -1,6 +1,7 @@
 """GPU parity of the cache (srt_trie_insert / srt_trie_export) against the
 oracle's substring counts, bit-exact: full inserts, chunked online inserts,
-order independence, and the sticky error flags."""
+order independence, depths 1, 2 and 64, segments longer than a workgroup,
+and the sticky error flags."""
 import random
 
 import numpy as np
@@ -123,3 +124,34 @@ def test_export_truncation_reports_capacity():
     with pytest.raises(srt.SrtError) as e:
         srt.srt_trie_export(c.ws, 0, 4)
     assert e.value.status == srt.SRT_ERR_CAPACITY
+
+
+@pytest.mark.parametrize("D,chunks", [(64, 9), (64, None), (1, 5), (2, None)])
+def test_depth_extremes(D, chunks):
+    # D = 64: every stream keeps 63 active nodes between chunks; D = 1 and 2:
+    # none or one
+    rng = random.Random(D * 7 + (chunks or 0))
+    streams = [[np.array([rng.randrange(3) for _ in range(rng.randrange(0, 150))]) for _ in range(4)]
+               for _ in range(2)]
+    say(f"cache: depth extremes D={D} chunks={chunks}")
+    c = build(streams, D, chunks=chunks, rng=rng)
+    assert c.status()["flags"] == 0
+    for p in range(2):
+        check_prompt(c, p, streams[p], D)
+
+
+def test_segments_longer_than_a_workgroup():
+    # one call appends 3000 tokens to a stream (more substring starts than
+    # threads in the workgroup) and 1100 tokens to another that already has
+    # active nodes
+    rng = random.Random(99)
+    D = 6
+    s0 = np.array([rng.randrange(5) for _ in range(3000)])
+    s1 = np.array([rng.randrange(5) for _ in range(1300)])
+    c = Caches.create(1, 4, D, (len(s0) + len(s1)) * D + 64)
+    ids = c.new_streams(2)
+    say("cache: 3000- and 1100-token segments")
+    c.insert([0], ids[1:], [s1[:200]])
+    c.insert([0, 0], ids, [s0, s1[200:]])
+    assert c.status()["flags"] == 0
+    check_prompt(c, 0, [s0, s1], D)
