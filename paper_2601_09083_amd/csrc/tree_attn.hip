@@ -28,7 +28,8 @@
 //     reads of every MFMA are bank-conflict free and their addresses are one
 //     base register plus immediate offsets.
 //   * Softmax uses exp2 with scale*log2(e) folded in and a lazily raised
-//     reference maximum.  The ancestor mask is a bitset per tree node in LDS;
+//     reference maximum; a tile whose probabilities all stay below 2^8 of
+//     the reference (checked on their sum) needs no row maximum at all.  The ancestor mask is a bitset per tree node in LDS;
 //     on tiles that reach the tree positions or the end of the range each
 //     row takes a 64-bit visibility window of it (two LDS words) and masks
 //     its scores bit by bit.
@@ -234,6 +235,13 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
         reinterpret_cast<const bf16x8*>(a.q + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + hq) * D + 8 * h);
 #pragma unroll
     for (int ks = 0; ks < Sh::KS; ++ks) qf[ks] = row_ok ? qp[2 * ks] : bf16x8{};
+    // Scores come out of the product already in log2 units: each query
+    // element is multiplied by scale*log2(e) and rounded back to bf16.
+    const float cq = a.scale_log2;
+#pragma unroll
+    for (int ks = 0; ks < Sh::KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[ks][e] = static_cast<__bf16>(static_cast<float>(qf[ks][e]) * cq);
   }
 
   f32x16 o[Sh::DB];
@@ -247,7 +255,6 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   constexpr float kLazy = 8.f;
   float m = -INFINITY;
   float l = 0.f;
-  const float c = a.scale_log2;
 
   // ---- staging ----------------------------------------------------------
   // Wave w moves keys 8w .. 8w+7 of every K and V tile; they lie inside one
@@ -309,8 +316,9 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   const int xg = lane % 16;
   const int k_vd = (4 * h + xg / 4) * Sh::VSTRIDE + ((CPR / 2) * ((lane / 16) & 1) + (xg % 4) / 2) * 16 + 8 * (xg & 1);
 
-  // S^T[key][row] of one tile: two 32-key blocks.
-  auto qk = [&](const uint8_t* Kb, f32x16 (&sacc)[2]) {
+  // S^T[key][row] - mref of one tile (log2 units): two 32-key blocks, the
+  // accumulators seeded with seed = -mref.
+  auto qk = [&](const uint8_t* Kb, f32x16 (&sacc)[2], float seed) {
     // All fragment reads are issued before the first MFMA so that one LDS
     // latency, not one per k-step, is exposed.
     bf16x8 kf[Sh::KS][2];
@@ -322,7 +330,7 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = seed;
 #pragma unroll
     for (int ks = 0; ks < Sh::KS; ++ks)
 #pragma unroll
@@ -334,7 +342,7 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
 
   // Mask, online softmax with lazy rescale; returns P in bf16.  Lane holds
   // keys 32 kb + 8 (r/4) + 4 h + r%4 of its row in sacc[kb][r].
-  auto softmax = [&](int t0, f32x16 (&sacc)[2], bf16x8 (&pb)[4]) {
+  auto softmax = [&](int t0, f32x16 (&sacc)[2], bf16x8 (&pb)[4], float mref0) {
     const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
     if (need_mask) {
       // Visibility of keys t0 .. t0+63 for this lane's row as one 64-bit
@@ -371,48 +379,59 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
         }
       }
     }
-    // (maximum, not fmaxf: no NaN-quieting of every operand; scores are
-    // finite or -inf)
-    float mloc = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; r += 2)
-        mloc = __builtin_elementwise_maximum(mloc, __builtin_elementwise_maximum(sacc[kb][r], sacc[kb][r + 1]));
-    mloc = max_halves(mloc);
-    const float ms = mloc * c;  // row max in log2 units (c > 0)
-    const bool raise = ms > m + kLazy;
-    if (__ballot(raise)) {
-      const float mnew = raise ? ms : m;
-      const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mnew);
-      l *= alpha;
-#pragma unroll
-      for (int db = 0; db < Sh::DB; ++db) o[db] *= alpha;
-      m = mnew;
-    }
-    const float mref = m == -INFINITY ? 0.f : m;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][r], c, -mref));
+    // Probabilities exp2(score - mref0 - dm), rounded to bf16 for the second
+    // product (sacc holds score - mref0); returns this lane's sum of them
+    // (its 32 keys of the row, two bf16 pairs per dot2, two accumulators).
     // Contraction index 8 h + e of k-step ks <-> key 16 ks + 8 (e/4) + 4 h + e%4.
+    auto probs = [&](auto dm_c, float dm) {
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      const bf16x2 one2 = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+      float ps[2] = {0.f, 0.f};
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
+      for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pb[ks][e] = static_cast<__bf16>(sacc[ks / 2][8 * (ks % 2) + e]);
-    // Row sum of the probabilities as rounded for the second product (two
-    // bf16 pairs per dot2, two accumulators).
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    const bf16x2 one2 = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
-    float ps[2] = {0.f, 0.f};
+        for (int e = 0; e < 8; ++e)
+          pb[ks][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(
+              decltype(dm_c)::value ? sacc[ks / 2][8 * (ks % 2) + e] - dm : sacc[ks / 2][8 * (ks % 2) + e]));
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int e = 0; e < 8; e += 2) {
-        const bf16x2 pr = {pb[ks][e], pb[ks][e + 1]};
-        ps[ks & 1] = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, ps[ks & 1], false);
+        for (int e = 0; e < 8; e += 2) {
+          const bf16x2 pr = {pb[ks][e], pb[ks][e + 1]};
+          ps[ks & 1] = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, ps[ks & 1], false);
+        }
       }
-    l += ps[0] + ps[1];
+      return ps[0] + ps[1];
+    };
+    // Fast path: exponentiate against the current reference without first
+    // taking the row maximum.  If every rounded probability of the row is
+    // below 2^kLazy (their sum is), no score exceeds the reference by kLazy,
+    // so the reference would not be raised and these are the final values.
+    // Otherwise (or while the reference is still -inf) the wave takes the
+    // row maximum, raises the reference as needed and exponentiates again.
+    float psum = probs(std::false_type(), 0.f);
+    const bool fast = m != -INFINITY && psum < 256.f;  // 256 = 2^kLazy
+    if (__ballot(!fast)) {
+      // (maximum, not fmaxf: no NaN-quieting of every operand; scores are
+      // finite or -inf)
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; r += 2)
+          mloc = __builtin_elementwise_maximum(mloc, __builtin_elementwise_maximum(sacc[kb][r], sacc[kb][r + 1]));
+      mloc = max_halves(mloc);
+      const float ms = mloc + mref0;  // row max in log2 units
+      const bool raise = ms > m + kLazy;
+      if (__ballot(raise)) {
+        const float mnew = raise ? ms : m;
+        const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mnew);
+        l *= alpha;
+#pragma unroll
+        for (int db = 0; db < Sh::DB; ++db) o[db] *= alpha;
+        m = mnew;
+      }
+      psum = probs(std::true_type(), (m == -INFINITY ? 0.f : m) - mref0);
+    }
+    l += psum;
   };
 
   // O^T[d][row] += V^T P^T.
@@ -465,13 +484,14 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
     }
     if (wave_active) {
       f32x16 sacc[2];
-      qk(Ks + cur * Sh::KTILE, sacc);
+      const float mref0 = m == -INFINITY ? 0.f : m;
+      qk(Ks + cur * Sh::KTILE, sacc, -mref0);
       // First half of the V^T fragments is read while softmax runs, the
       // second half while the first half's MFMAs run.
       i16x4v vf0[2][Sh::DB][2], vf1[2][Sh::DB][2];
       v_read(Vs + cur * Sh::VTILE, 0, vf0);
       bf16x8 pb[4];
-      softmax(t0, sacc, pb);
+      softmax(t0, sacc, pb, mref0);
       v_read(Vs + cur * Sh::VTILE, 2, vf1);
       pv(vf0, 0, pb);
       pv(vf1, 2, pb);
