@@ -16,8 +16,11 @@
  *
  * Conventions shared by every entry point
  *   - Pointers are device pointers unless the comment says "host".  All
- *     device memory is owned by the caller; the library allocates nothing
- *     and keeps no global state.
+ *     device memory is owned by the caller and the library allocates
+ *     nothing.  The only state kept between calls is a per-device cache of
+ *     the compute-unit count (read once per device, used to size the
+ *     persistent attention grid); no call's results depend on an earlier
+ *     call except through the buffers the caller passes.
  *   - `stream` is a hipStream_t passed as void* (NULL = default stream).
  *     Every call only enqueues work on it and returns, except those marked
  *     "synchronises".  Calls sharing a workspace must be ordered on one
@@ -162,7 +165,9 @@ int srt_draft(const void* ws, int32_t B, const int32_t* prompt_ids, const int32_
  * i < n_nodes[b]:
  *   keys = positions [0, L) and L + j for every ancestor-or-self j of i,
  *   L = ctx_len[b]; position p lives in page block_table[b, p / page],
- *   slot p % page;  out[b,i,h,:] = softmax(scale * q.K^T) V.
+ *   slot p % page;  out[b,i,h,:] = softmax(scale * q.K^T) V, with q and K
+ *   used exactly as given (fp32 dot products, the scale applied to them).
+ *   scale must be finite (else SRT_ERR_INVALID).
  * Layouts (bf16 bits): q, out [B, N, Hq, d]; k_cache, v_cache
  *   [num_pages, Hkv, page, d]; block_table [B, max_pages] int32;
  *   ctx_len, n_nodes [B] int32; tree_parent [B, N] int32 as from srt_draft.

@@ -27,9 +27,10 @@
 //     LDS.  LDS rows are padded (K by 16 bytes, V by 32) so that the operand
 //     reads of every MFMA are bank-conflict free and their addresses are one
 //     base register plus immediate offsets.
-//   * Softmax uses exp2 with scale*log2(e) folded in and a lazily raised
-//     reference maximum; a tile whose probabilities all stay below 2^8 of
-//     the reference (checked on their sum) needs no row maximum at all.  The ancestor mask is a bitset per tree node in LDS;
+//   * Softmax uses exp2 of fma(q.k, scale*log2(e), -reference) (Q is never
+//     rescaled or re-rounded) and a lazily raised reference maximum; a tile
+//     whose probabilities all stay below 2^8 of the reference (checked on
+//     their sum) needs no row maximum at all.  The ancestor mask is a bitset per tree node in LDS;
 //     on tiles that reach the tree positions or the end of the range each
 //     row takes a 64-bit visibility window of it (two LDS words) and masks
 //     its scores bit by bit.
@@ -235,14 +236,11 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
         reinterpret_cast<const bf16x8*>(a.q + ((static_cast<int64_t>(b) * a.N + node) * a.Hq + hq) * D + 8 * h);
 #pragma unroll
     for (int ks = 0; ks < Sh::KS; ++ks) qf[ks] = row_ok ? qp[2 * ks] : bf16x8{};
-    // Scores come out of the product already in log2 units: each query
-    // element is multiplied by scale*log2(e) and rounded back to bf16.
-    const float cq = a.scale_log2;
-#pragma unroll
-    for (int ks = 0; ks < Sh::KS; ++ks)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[ks][e] = static_cast<__bf16>(static_cast<float>(qf[ks][e]) * cq);
+    // Q is used exactly as given: the scale is applied to the fp32 scores
+    // (rounding a scaled Q back to bf16 would perturb every score by up to
+    // 2^-9 of its magnitude).
   }
+  const float c_log2 = a.scale_log2;  // scale * log2(e)
 
   f32x16 o[Sh::DB];
 #pragma unroll
@@ -316,9 +314,9 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   const int xg = lane % 16;
   const int k_vd = (4 * h + xg / 4) * Sh::VSTRIDE + ((CPR / 2) * ((lane / 16) & 1) + (xg % 4) / 2) * 16 + 8 * (xg & 1);
 
-  // S^T[key][row] - mref of one tile (log2 units): two 32-key blocks, the
-  // accumulators seeded with seed = -mref.
-  auto qk = [&](const uint8_t* Kb, f32x16 (&sacc)[2], float seed) {
+  // S^T[key][row] = q . k of one tile (raw fp32 dot products): two 32-key
+  // blocks.
+  auto qk = [&](const uint8_t* Kb, f32x16 (&sacc)[2]) {
     // All fragment reads are issued before the first MFMA so that one LDS
     // latency, not one per k-step, is exposed.
     bf16x8 kf[Sh::KS][2];
@@ -330,7 +328,7 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = seed;
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < Sh::KS; ++ks)
 #pragma unroll
@@ -343,6 +341,13 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
   // Mask, online softmax with lazy rescale; returns P in bf16.  Lane holds
   // keys 32 kb + 8 (r/4) + 4 h + r%4 of its row in sacc[kb][r].
   auto softmax = [&](int t0, f32x16 (&sacc)[2], bf16x8 (&pb)[4], float mref0) {
+    // Scores in log2 units relative to the reference: q.k * scale * log2(e)
+    // - mref0, one fp32 fused multiply-add per score (masked scores are set
+    // to -inf afterwards, so any finite scale is safe).
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = __builtin_fmaf(sacc[kb][r], c_log2, -mref0);
     const bool need_mask = (t0 + kTile > si.L) || (t0 + kTile > k_end);
     if (need_mask) {
       // Visibility of keys t0 .. t0+63 for this lane's row as one 64-bit
@@ -485,7 +490,7 @@ __global__ __launch_bounds__(kThreads, 1) void tree_attn_kernel(AttnArgs a) {
     if (wave_active) {
       f32x16 sacc[2];
       const float mref0 = m == -INFINITY ? 0.f : m;
-      qk(Ks + cur * Sh::KTILE, sacc, -mref0);
+      qk(Ks + cur * Sh::KTILE, sacc);
       // First half of the V^T fragments is read while softmax runs, the
       // second half while the first half's MFMAs run.
       i16x4v vf0[2][Sh::DB][2], vf1[2][Sh::DB][2];
@@ -744,7 +749,7 @@ extern "C" int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int3
                              void* scratch, size_t scratch_bytes, void* stream) {
   if (B < 0 || N < 1 || N > kMaxN || Hq < 1 || Hkv < 1 || Hq % Hkv || page < 1 || max_pages < 1 || num_pages < 1)
     return SRT_ERR_INVALID;
-  if (!(scale == scale)) return SRT_ERR_INVALID;
+  if (!std::isfinite(scale)) return SRT_ERR_INVALID;
   if (d != 64 && d != 128) return SRT_ERR_UNSUPPORTED;
   if (page < 16 || (page & (page - 1))) return SRT_ERR_UNSUPPORTED;
   // work-list packing: sequence < 65536, KV head < 256, split < 4096,

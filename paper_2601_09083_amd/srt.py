@@ -8,6 +8,7 @@ library is missing, every call raises.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from typing import Optional
@@ -92,6 +93,13 @@ def _stream(stream=None):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _on(stream):
+    """Context in which buffers the binding allocates for a call belong to
+    the stream the call is enqueued on: torch's caching allocator then never
+    hands them out again while that stream may still use them."""
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
+
+
 def _ptr(t: Optional[torch.Tensor], dtype=None, name="tensor"):
     if t is None:
         return None
@@ -166,10 +174,11 @@ def srt_draft(ws: torch.Tensor, prompt_ids, ctx_tail, ctx_len, max_match: int, m
         raise ValueError("ctx_tail must be [B, max_match]")
     dev = prompt_ids.device
     if out is None:
-        out = {k: torch.empty((B, max_nodes), dtype=torch.int32, device=dev)
-               for k in ("tree_tokens", "tree_parent", "tree_depth")}
-        out["n_nodes"] = torch.empty(B, dtype=torch.int32, device=dev)
-        out["match_len"] = torch.empty(B, dtype=torch.int32, device=dev)
+        with _on(stream):
+            out = {k: torch.empty((B, max_nodes), dtype=torch.int32, device=dev)
+                   for k in ("tree_tokens", "tree_parent", "tree_depth")}
+            out["n_nodes"] = torch.empty(B, dtype=torch.int32, device=dev)
+            out["match_len"] = torch.empty(B, dtype=torch.int32, device=dev)
     prm = DraftParams(max_match, max_nodes, max_depth, int(bool(chain)), float(budget_alpha), float(min_score))
     _check("srt_draft", lib().srt_draft(
         _ptr(ws, torch.uint8, "ws"), B, _ptr(prompt_ids, torch.int32, "prompt_ids"),
@@ -194,11 +203,12 @@ def srt_tree_attn(q, k_cache, v_cache, block_table, ctx_len, tree_parent, n_node
     if d2 != d or v_cache.shape != k_cache.shape:
         raise ValueError("cache shape mismatch")
     max_pages = int(block_table.shape[1])
-    if out is None:
-        out = torch.empty_like(q)
     need = srt_tree_attn_scratch_bytes(B, N, Hq, Hkv, d, page, max_pages)
-    if need and (scratch is None or scratch.numel() < need):
-        scratch = torch.empty(need, dtype=torch.uint8, device=q.device)
+    with _on(stream):
+        if out is None:
+            out = torch.empty_like(q)
+        if need and (scratch is None or scratch.numel() < need):
+            scratch = torch.empty(need, dtype=torch.uint8, device=q.device)
     _check("srt_tree_attn", lib().srt_tree_attn(
         B, N, Hq, Hkv, d, page, max_pages, P, _ptr(q, torch.bfloat16, "q"), _ptr(k_cache, torch.bfloat16, "k_cache"),
         _ptr(v_cache, torch.bfloat16, "v_cache"), _ptr(block_table, torch.int32, "block_table"),
@@ -209,6 +219,13 @@ def srt_tree_attn(q, k_cache, v_cache, block_table, ctx_len, tree_parent, n_node
 
 
 # --------------------------------------------------------------------------- acceptance
+
+def _walk_outputs(B: int, max_depth: int, dev) -> dict:
+    return {"n_accepted": torch.empty(B, dtype=torch.int32, device=dev),
+            "out_tokens": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
+            "out_nodes": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
+            "n_emitted": torch.empty(B, dtype=torch.int32, device=dev)}
+
 
 def srt_accept_scratch_bytes(B: int) -> int:
     return int(lib().srt_accept_scratch_bytes(B))
@@ -221,14 +238,12 @@ def srt_accept(logits, gumbel, inv_temperature: float, tree_tokens, tree_parent,
     if gumbel is not None and tuple(gumbel.shape) != (B, max_depth + 1, V):
         raise ValueError("gumbel must be [B, max_depth+1, V]")
     dev = logits.device
-    if out is None:
-        out = {"n_accepted": torch.empty(B, dtype=torch.int32, device=dev),
-               "out_tokens": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
-               "out_nodes": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
-               "n_emitted": torch.empty(B, dtype=torch.int32, device=dev)}
     need = srt_accept_scratch_bytes(B)
-    if scratch is None or scratch.numel() < need:
-        scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    with _on(stream):
+        if out is None:
+            out = _walk_outputs(B, max_depth, dev)
+        if scratch is None or scratch.numel() < need:
+            scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     _check("srt_accept", lib().srt_accept(
         B, N, V, max_depth, _ptr(logits, torch.float32, "logits"), _ptr(gumbel, torch.float32, "gumbel"),
         float(inv_temperature), _ptr(tree_tokens, torch.int32, "tree_tokens"),
@@ -256,14 +271,12 @@ def srt_accept_lmhead(hidden, w_head, gumbel, inv_temperature: float, tree_token
     if tuple(tree_tokens.shape) != (B, N) or tuple(tree_parent.shape) != (B, N):
         raise ValueError("tree arrays must be [B, N]")
     dev = hidden.device
-    if out is None:
-        out = {"n_accepted": torch.empty(B, dtype=torch.int32, device=dev),
-               "out_tokens": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
-               "out_nodes": torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
-               "n_emitted": torch.empty(B, dtype=torch.int32, device=dev)}
     need = srt_accept_lmhead_scratch_bytes(B, N, V)
-    if scratch is None or scratch.numel() < need:
-        scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    with _on(stream):
+        if out is None:
+            out = _walk_outputs(B, max_depth, dev)
+        if scratch is None or scratch.numel() < need:
+            scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     _check("srt_accept_lmhead", lib().srt_accept_lmhead(
         B, N, dm, V, max_depth, _ptr(hidden, torch.bfloat16, "hidden"), _ptr(w_head, torch.bfloat16, "w_head"),
         _ptr(gumbel, torch.float32, "gumbel"), float(inv_temperature),
