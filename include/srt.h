@@ -19,8 +19,9 @@
  *     device memory is owned by the caller and the library allocates
  *     nothing.  The only state kept between calls is a per-device cache of
  *     the compute-unit count (read once per device, used to size the
- *     persistent attention grid); no call's results depend on an earlier
- *     call except through the buffers the caller passes.
+ *     persistent attention grid) and, for srt_accept_noalloc only, a fixed
+ *     per-device scratch array and its address; no call's results depend on
+ *     an earlier call except through the buffers the caller passes.
  *   - `stream` is a hipStream_t passed as void* (NULL = default stream).
  *     Every call only enqueues work on it and returns, except those marked
  *     "synchronises".  Calls sharing a workspace must be ordered on one
@@ -232,6 +233,31 @@ int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logit
                const int32_t* tree_parent, const int32_t* n_nodes, int32_t* n_accepted,
                int32_t* out_tokens, int32_t* out_nodes, int32_t* n_emitted, void* scratch,
                size_t scratch_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * srt_accept for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ *
+ * The same walk, arguments, outputs and results as srt_accept, bit for bit,
+ * without the scratch argument: the per-level walker lists, current nodes
+ * and candidates live in one fixed device array inside the library (about
+ * 2.1 MB, sized for SRT_ACCEPT_NOALLOC_MAX_BATCH sequences), which every GPU
+ * the library runs on holds until the process ends.  Its address is looked
+ * up once per device on the first call made with that device current; the
+ * call allocates nothing and calls no allocating routine.  B larger than
+ * SRT_ACCEPT_NOALLOC_MAX_BATCH returns SRT_ERR_CAPACITY before anything is
+ * enqueued; a failed address lookup returns SRT_ERR_HIP.  The array keeps
+ * the last call's contents (every call resets the counters it needs itself).
+ * All calls on one GPU share the array: calls that may overlap on one GPU
+ * (different streams without ordering between them) race and must not be
+ * issued.
+ * ---------------------------------------------------------------------- */
+#define SRT_ACCEPT_NOALLOC_MAX_BATCH 4096
+
+int srt_accept_noalloc(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits,
+                       const float* gumbel, float inv_temperature, const int32_t* tree_tokens,
+                       const int32_t* tree_parent, const int32_t* n_nodes, int32_t* n_accepted,
+                       int32_t* out_tokens, int32_t* out_nodes, int32_t* n_emitted, void* stream);
 
 /* ------------------------------------------------------------------------
  * Acceptance walk with the LM head applied at the visited nodes only

@@ -35,6 +35,7 @@
 #include <algorithm>
 #include <cfloat>
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 
@@ -75,13 +76,14 @@ struct ScratchLayout {
   size_t off_act, off_cur, off_cand, total;
 };
 
-inline ScratchLayout scratch_layout(int64_t B) {
-  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
-  ScratchLayout s;
-  s.off_act = up(sizeof(int32_t) * (kMaxLevels + 1));
-  s.off_cur = s.off_act + up(sizeof(int32_t) * 2 * static_cast<size_t>(B));
-  s.off_cand = s.off_cur + up(sizeof(int32_t) * 2 * static_cast<size_t>(B));
-  s.total = s.off_cand + up(sizeof(unsigned long long) * 2 * static_cast<size_t>(B) * kMaxChunks);
+constexpr size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
+
+constexpr ScratchLayout scratch_layout(int64_t B) {
+  ScratchLayout s{};
+  s.off_act = round256(sizeof(int32_t) * (kMaxLevels + 1));
+  s.off_cur = s.off_act + round256(sizeof(int32_t) * 2 * static_cast<size_t>(B));
+  s.off_cand = s.off_cur + round256(sizeof(int32_t) * 2 * static_cast<size_t>(B));
+  s.total = s.off_cand + round256(sizeof(unsigned long long) * 2 * static_cast<size_t>(B) * kMaxChunks);
   return s;
 }
 
@@ -277,26 +279,26 @@ __global__ __launch_bounds__(kWalkWaves * SRT_WAVE) void accept_walk_kernel(Acce
   if (lane == 0) record(a, b, level, st);
 }
 
-}  // namespace
-
-extern "C" size_t srt_accept_scratch_bytes(int32_t B) {
-  if (B < 0) return 0;
-  return scratch_layout(std::max(B, 1)).total;
-}
-
-extern "C" int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits, const float* gumbel,
-                          float inv_temperature, const int32_t* tree_tokens, const int32_t* tree_parent,
-                          const int32_t* n_nodes, int32_t* n_accepted, int32_t* out_tokens, int32_t* out_nodes,
-                          int32_t* n_emitted, void* scratch, size_t scratch_bytes, void* stream) {
+// Host checks shared by both entry points (before any scratch is touched).
+int check_args(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits, float inv_temperature,
+               const int32_t* tree_tokens, const int32_t* tree_parent, const int32_t* n_nodes,
+               const int32_t* n_accepted, const int32_t* out_tokens, const int32_t* out_nodes) {
   if (B < 0 || N < 1 || N > kMaxN || V < 1 || Dmax < 0 || Dmax >= kMaxLevels) return SRT_ERR_INVALID;
   if (!(inv_temperature == inv_temperature)) return SRT_ERR_INVALID;
   if (B == 0) return SRT_OK;
   if (!logits || !tree_tokens || !tree_parent || !n_nodes || !n_accepted || !out_tokens || !out_nodes)
     return SRT_ERR_INVALID;
-  if (!scratch || scratch_bytes < srt_accept_scratch_bytes(B)) return SRT_ERR_CAPACITY;
-  if (reinterpret_cast<uintptr_t>(scratch) % 256) return SRT_ERR_INVALID;
+  return SRT_OK;
+}
+
+// The walk itself on scratch memory `base` (device, 256-byte aligned, at
+// least scratch_layout(B).total bytes); the init kernel resets the level
+// counters, so the scratch contents on entry do not matter.
+int launch_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits, const float* gumbel,
+                  float inv_temperature, const int32_t* tree_tokens, const int32_t* tree_parent,
+                  const int32_t* n_nodes, int32_t* n_accepted, int32_t* out_tokens, int32_t* out_nodes,
+                  int32_t* n_emitted, char* base, void* stream) {
   const ScratchLayout L = scratch_layout(B);
-  char* base = static_cast<char*>(scratch);
   AcceptArgs a;
   a.logits = logits;
   a.gumbel = gumbel;
@@ -341,4 +343,68 @@ extern "C" int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const f
     st = launch_status();
   }
   return st;
+}
+
+// Scratch of srt_accept_noalloc: one fixed array per device, sized for
+// kNoAllocMaxB sequences, whose device address is looked up once per device
+// (hipGetSymbolAddress) and kept; host code never uses the array's name as
+// an address.
+constexpr int32_t kNoAllocMaxB = SRT_ACCEPT_NOALLOC_MAX_BATCH;
+constexpr int kMaxDevices = 64;
+std::mutex g_noalloc_mu;
+char* g_noalloc_ptr[kMaxDevices] = {};
+
+constexpr size_t kNoAllocBytes = scratch_layout(kNoAllocMaxB).total;  // 2,163,200 bytes
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+namespace {
+
+// Device address of this device's fixed scratch array (nullptr on error).
+char* noalloc_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  if (!g_noalloc_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_noalloc_ptr[dev] = static_cast<char*>(ptr);
+  }
+  return g_noalloc_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" size_t srt_accept_scratch_bytes(int32_t B) {
+  if (B < 0) return 0;
+  return scratch_layout(std::max(B, 1)).total;
+}
+
+extern "C" int srt_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits, const float* gumbel,
+                          float inv_temperature, const int32_t* tree_tokens, const int32_t* tree_parent,
+                          const int32_t* n_nodes, int32_t* n_accepted, int32_t* out_tokens, int32_t* out_nodes,
+                          int32_t* n_emitted, void* scratch_buf, size_t scratch_bytes, void* stream) {
+  int st = check_args(B, N, V, Dmax, logits, inv_temperature, tree_tokens, tree_parent, n_nodes, n_accepted,
+                      out_tokens, out_nodes);
+  if (st != SRT_OK || B == 0) return st;
+  if (!scratch_buf || scratch_bytes < srt_accept_scratch_bytes(B)) return SRT_ERR_CAPACITY;
+  if (reinterpret_cast<uintptr_t>(scratch_buf) % 256) return SRT_ERR_INVALID;
+  return launch_accept(B, N, V, Dmax, logits, gumbel, inv_temperature, tree_tokens, tree_parent, n_nodes,
+                       n_accepted, out_tokens, out_nodes, n_emitted, static_cast<char*>(scratch_buf), stream);
+}
+
+extern "C" int srt_accept_noalloc(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits,
+                                  const float* gumbel, float inv_temperature, const int32_t* tree_tokens,
+                                  const int32_t* tree_parent, const int32_t* n_nodes, int32_t* n_accepted,
+                                  int32_t* out_tokens, int32_t* out_nodes, int32_t* n_emitted, void* stream) {
+  int st = check_args(B, N, V, Dmax, logits, inv_temperature, tree_tokens, tree_parent, n_nodes, n_accepted,
+                      out_tokens, out_nodes);
+  if (st != SRT_OK || B == 0) return st;
+  if (B > kNoAllocMaxB) return SRT_ERR_CAPACITY;
+  char* base = noalloc_scratch();
+  if (!base) return SRT_ERR_HIP;
+  return launch_accept(B, N, V, Dmax, logits, gumbel, inv_temperature, tree_tokens, tree_parent, n_nodes,
+                       n_accepted, out_tokens, out_nodes, n_emitted, base, stream);
 }

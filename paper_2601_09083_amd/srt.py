@@ -27,7 +27,8 @@ _NAMES = {SRT_ERR_INVALID: "SRT_ERR_INVALID", SRT_ERR_CAPACITY: "SRT_ERR_CAPACIT
 EXPORTS = ("srt_trie_workspace_bytes", "srt_trie_init", "srt_trie_insert", "srt_trie_reset_streams",
            "srt_trie_status", "srt_trie_export", "srt_draft", "srt_tree_attn_scratch_bytes",
            "srt_tree_attn", "srt_accept_scratch_bytes", "srt_accept", "srt_accept_lmhead_scratch_bytes",
-           "srt_accept_lmhead", "srt_commit", "srt_version")
+           "srt_accept_lmhead", "srt_commit", "srt_version", "srt_accept_noalloc")
+SRT_ACCEPT_NOALLOC_MAX_BATCH = 4096  # include/srt.h
 
 
 class SrtError(RuntimeError):
@@ -71,6 +72,7 @@ def lib() -> ctypes.CDLL:
             "srt_tree_attn": (ctypes.c_int, [_I32] * 7 + [_I64] + [_P] * 7 + [ctypes.c_float, _P, _P, _SZ, _P]),
             "srt_accept_scratch_bytes": (_SZ, [_I32]),
             "srt_accept": (ctypes.c_int, [_I32] * 4 + [_P, _P, ctypes.c_float] + [_P] * 7 + [_P, _SZ, _P]),
+            "srt_accept_noalloc": (ctypes.c_int, [_I32] * 4 + [_P, _P, ctypes.c_float] + [_P] * 7 + [_P]),
             "srt_accept_lmhead_scratch_bytes": (_SZ, [_I32, _I32, _I32]),
             "srt_accept_lmhead": (ctypes.c_int, [_I32] * 5 + [_P, _P, _P, ctypes.c_float] + [_P] * 7 + [_P, _SZ, _P]),
             "srt_commit": (ctypes.c_int, [_I32] * 6 + [_I64] + [_P] * 4 + [_I32] + [_P] * 3 + [_I32, _P, _P, _P]),
@@ -251,6 +253,23 @@ def srt_accept(logits, gumbel, inv_temperature: float, tree_tokens, tree_parent,
         _ptr(out["n_accepted"], torch.int32), _ptr(out["out_tokens"], torch.int32),
         _ptr(out["out_nodes"], torch.int32), _ptr(out.get("n_emitted"), torch.int32), _ptr(scratch, name="scratch"),
         scratch.numel(), _stream(stream)))
+    return out
+
+
+def srt_accept_noalloc(logits, gumbel, inv_temperature: float, tree_tokens, tree_parent, n_nodes, max_depth: int,
+                       out, stream=None) -> dict:
+    """srt_accept with the library's fixed per-device scratch array: the
+    caller passes preallocated outputs (``out`` as srt_accept returns it) and
+    nothing is allocated, here or in the library.  B <= 4096."""
+    B, N, V = logits.shape
+    if gumbel is not None and tuple(gumbel.shape) != (B, max_depth + 1, V):
+        raise ValueError("gumbel must be [B, max_depth+1, V]")
+    _check("srt_accept_noalloc", lib().srt_accept_noalloc(
+        B, N, V, max_depth, _ptr(logits, torch.float32, "logits"), _ptr(gumbel, torch.float32, "gumbel"),
+        float(inv_temperature), _ptr(tree_tokens, torch.int32, "tree_tokens"),
+        _ptr(tree_parent, torch.int32, "tree_parent"), _ptr(n_nodes, torch.int32, "n_nodes"),
+        _ptr(out["n_accepted"], torch.int32), _ptr(out["out_tokens"], torch.int32),
+        _ptr(out["out_nodes"], torch.int32), _ptr(out.get("n_emitted"), torch.int32), _stream(stream)))
     return out
 
 

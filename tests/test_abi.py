@@ -178,3 +178,22 @@ def test_host_validation_before_any_hip_call():
     assert L.srt_commit(*com) == S.SRT_ERR_INVALID                   # ctx_tail without draft_len
     com[0] = 0; com[16] = None
     assert L.srt_commit(*com) == S.SRT_OK                            # B = 0
+
+
+def test_accept_noalloc_rejects_batches_beyond_its_array():
+    """Host checks of srt_accept_noalloc, before any device memory is
+    touched: a batch above SRT_ACCEPT_NOALLOC_MAX_BATCH is SRT_ERR_CAPACITY,
+    B = 0 is a no-op, invalid sizes are SRT_ERR_INVALID.  (The pointers are
+    never dereferenced on these paths.)"""
+    L = S.lib()
+    fake = ctypes.c_void_p(0x1000)
+    args = lambda B, N=8, V=100, Dmax=4: (B, N, V, Dmax, fake, None, 1.0, fake, fake, fake, fake, fake, fake, None,
+                                          None)
+    assert S.SRT_ACCEPT_NOALLOC_MAX_BATCH == 4096
+    hdr = open(HEADER).read()
+    assert re.search(r"#define SRT_ACCEPT_NOALLOC_MAX_BATCH 4096\b", hdr)
+    assert L.srt_accept_noalloc(*args(4097)) == S.SRT_ERR_CAPACITY
+    assert L.srt_accept_noalloc(*args(1 << 30)) == S.SRT_ERR_CAPACITY
+    assert L.srt_accept_noalloc(*args(0)) == S.SRT_OK
+    assert L.srt_accept_noalloc(*args(4, N=0)) == S.SRT_ERR_INVALID
+    assert L.srt_accept_noalloc(*args(4, Dmax=64)) == S.SRT_ERR_INVALID
