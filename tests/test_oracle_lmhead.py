@@ -125,6 +125,40 @@ def test_error_bound_covers_other_orders():
     assert worst > 0.0  # the orders do differ from the oracle somewhere
 
 
+def _seq32(p):
+    s = np.float32(0)
+    for x in p:
+        s = np.float32(s + x)
+    return s
+
+
+@pytest.mark.parametrize("d", [64, 1024, 3584])
+def test_error_bound_is_tight_on_a_worst_case_order(d):
+    """Closed-form worst case: products 1, t, t, ..., t with t = 255 2^-32,
+    just below half an ulp of 1 (2^-24).  Sequential fp32 summation rounds
+    every addition down, so it returns exactly 1; the exact sum is
+    1 + (d - 1) t and the oracle rounds that once.  The observed error is
+    therefore known, and the bound must cover it while staying within its
+    own safety factor of 2 (plus the one rounding term): a bound inflated by
+    a few percent, or one that ignored the (d - 1) additions, fails here."""
+    h = np.full(d, np.float32(255 * 2.0 ** -20), dtype=np.float32)  # 255/256 * 2^-12: bf16
+    h[0] = 1.0
+    W = np.full((1, d), np.float32(2.0 ** -12), dtype=np.float32)
+    W[0, 0] = 1.0
+    assert np.array_equal(bf16_round(h), h) and np.array_equal(bf16_round(W), W)
+    prods = (W[0] * h).astype(np.float32)
+    t = np.float32(255 * 2.0 ** -32)
+    assert prods[0] == 1.0 and (prods[1:] == t).all() and t < 2.0 ** -24
+    assert _seq32(prods) == np.float32(1.0)  # every addition rounds down
+    exact = Fraction(1) + (d - 1) * Fraction(255, 2 ** 32)
+    ref = LH.head_logits(h, W)[0]
+    assert ref == np.float32(float(exact))  # one rounding of the exact sum
+    err = float(ref) - 1.0
+    assert err > 0.0
+    bound = float(LH.logit_error_bound(h, W)[0])
+    assert err <= bound <= 2.05 * err, (d, err, bound, bound / err)
+
+
 def test_planted_mistakes_fail():
     rng = np.random.default_rng(7)
     V, d, N, Dmax = 24, 24, 10, 4
