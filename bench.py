@@ -34,7 +34,9 @@ sys.path.insert(0, ROOT)
 METRIC = "verified draft-tree tokens/sec + tree-attn HBM GB/s (% peak) at 1 GPU"
 HBM_PEAK_GBPS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
-COUNTERS = os.path.join(ROOT, "profiles", "tree_attn_qwen7b_counters.json")
+def counters_path(config_name):
+    """Committed rocprofv3 HBM-counter summary of srt_tree_attn on one workload."""
+    return os.path.join(ROOT, "profiles", f"tree_attn_{config_name.replace('.', 'p')}_counters.json")
 ATTN_SRC = os.path.join(ROOT, "paper_2601_09083_amd", "csrc", "tree_attn.hip")
 
 
@@ -57,13 +59,14 @@ def source_sha(path):
     return hashlib.sha256(open(path, "rb").read()).hexdigest()
 
 
-def counter_traffic():
+def counter_traffic(config_name):
     """HBM bytes per launch from committed rocprofv3 counters, if they were
     taken on the current kernel source."""
-    if not os.path.exists(COUNTERS):
+    path = counters_path(config_name)
+    if not os.path.exists(path):
         return None
     try:
-        c = json.load(open(COUNTERS))
+        c = json.load(open(path))
         if c.get("source_sha256") != source_sha(ATTN_SRC):
             return None
         return c.get("hbm_bytes_per_launch")
@@ -79,7 +82,7 @@ def _short_name(name):
     return n.split("(")[0]
 
 
-def write_counter_file(d):
+def write_counter_file(d, config_name):
     """HBM traffic per srt_tree_attn launch from four rocprofv3 --pmc runs in
     directory d: pmc_FETCH_SIZE / pmc_WRITE_SIZE of `bench.py --no-cpu-baseline
     --steps 5 --warmup 1` and pmc_copy_* of `bench.py --copy-calibration`.
@@ -96,7 +99,7 @@ def write_counter_file(d):
         return {k: [v for _, v in sorted(x)] for k, x in out.items()}
 
     res = {"source_sha256": source_sha(ATTN_SRC),
-           "kernel": "srt_tree_attn = " + " + ".join(ATTN_KERNELS) + " (Qwen2.5-7B-shaped workload)",
+           "kernel": "srt_tree_attn = " + " + ".join(ATTN_KERNELS) + f" ({config_name} workload)",
            "calibration": {}, "per_kernel_bytes": {}}
     per_launch = {}
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
@@ -118,7 +121,7 @@ def write_counter_file(d):
     alg = json.loads(line)["roofline"]["algorithmic_bytes"]
     res["algorithmic_bytes_per_launch"] = alg
     res["traffic_over_algorithmic"] = res["hbm_bytes_per_launch"] / alg
-    json.dump(res, open(COUNTERS, "w"), indent=1)
+    json.dump(res, open(counters_path(config_name), "w"), indent=1)
     print(json.dumps(res, indent=1))
 
 
@@ -254,6 +257,60 @@ def bulk_build(cfg, tw, reps: int = 2):
     torch.cuda.empty_cache()
     return {"tokens": total, "streams": len(streams), "ms": best, "tokens_per_s": total / (best / 1e3),
             "depth": cfg.trie_depth, "node_updates_per_s": total * cfg.trie_depth / (best / 1e3)}
+
+
+def full_tree_attention(st, cfg, n, calls: int = 10):
+    """srt_tree_attn with every tree forced to n nodes (random parents
+    among the 5 preceding nodes, so depths grow like drafted trees) on the
+    workload's own contexts and KV cache, timed with events around each of
+    ``calls`` launches after one warm-up.  Reported against both rooflines:
+    algorithmic bytes (context + tree K/V once, Q, O) and FLOPs (4 d per
+    (query row, visible key))."""
+    import torch
+
+    from paper_2601_09083_amd import srt
+
+    B, d, hq, hkv = st.tokens.batch, cfg.head_dim, cfg.hq, cfg.hkv
+    L = st.tokens.ctx_len.astype(np.int64)
+    cap = st.block_table.shape[1] * cfg.page
+    if int(L.max()) + n > cap:
+        return {"n": n, "skipped": "KV cache has no room for the tree"}
+    rng = np.random.default_rng(n)
+    par = np.full((B, n), -1, dtype=np.int32)
+    depth = np.zeros((B, n), dtype=np.int64)
+    for i in range(1, n):
+        par[:, i] = rng.integers(np.maximum(0, i - 5), i, size=B) if i > 0 else 0
+        depth[:, i] = depth[np.arange(B), par[:, i]] + 1
+    dev = st.q.device
+    q = torch.randn((B, n, hq, d), device=dev).to(torch.bfloat16)
+    out = torch.empty_like(q)
+    ctx = torch.as_tensor(st.tokens.ctx_len, device=dev)
+    tp = torch.as_tensor(par, device=dev)
+    nn = torch.full((B,), n, dtype=torch.int32, device=dev)
+    need = srt.srt_tree_attn_scratch_bytes(B, n, hq, hkv, d, cfg.page, st.block_table.shape[1])
+    scratch = torch.empty(need, dtype=torch.uint8, device=dev)
+    call = lambda: srt.srt_tree_attn(q, st.k_cache, st.v_cache, st.block_table, ctx, tp, nn, st.scale, out=out,
+                                     scratch=scratch)
+    call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        call()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    nbytes = float(((L + n) * hkv * d * 4).sum() + B * n * hq * d * 4)
+    flops = float(4 * d * hq * (n * L.sum() + (depth + 1).sum()))
+    tf = flops / (ms / 1e3) / 1e12
+    gbps = nbytes / (ms / 1e3) / 1e9
+    del q, out, scratch
+    torch.cuda.empty_cache()
+    bound = "mfma" if flops / (BF16_PEAK_TFLOPS * 1e12) >= nbytes / (HBM_PEAK_GBPS * 1e9) else "hbm"
+    return {"n": n, "ms": ms, "TFLOP/s": tf, "mfma_frac": tf / BF16_PEAK_TFLOPS, "GB/s": gbps,
+            "hbm_frac": gbps / HBM_PEAK_GBPS, "bound": bound, "flop_per_byte": flops / nbytes,
+            "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
 
 
 FINISH_ROWS = 128  # srt_accept_lmhead finishes the walks in one pass at or below this many subtree nodes
@@ -425,6 +482,12 @@ def main():
                     help="timed calls of the fused LM-head walk (0: skip it)")
     ap.add_argument("--no-unfused", action="store_true", help="skip timing the unfused LM head + walk")
     ap.add_argument("--no-bulk", action="store_true", help="skip timing the set-up bulk cache build")
+    ap.add_argument("--kv-pools", type=int, default=0,
+                    help="copies of the KV cache the steps rotate through (0: 3 when the cache fits in the "
+                         "256 MB Infinity Cache, else 1)")
+    ap.add_argument("--full-tree", default="64,256",
+                    help="tree sizes for the full-tree attention pass (every tree forced to that size), "
+                         "comma separated; empty to skip")
     ap.add_argument("--part-steps", type=int, default=20,
                     help="steps of the separate pass that times every part with its own events")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -433,7 +496,7 @@ def main():
                     help="write the attention HBM-traffic file from rocprofv3 --pmc runs in DIR and exit")
     args = ap.parse_args()
     if args.counters_from:
-        write_counter_file(args.counters_from)
+        write_counter_file(args.counters_from, args.config)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
@@ -467,12 +530,24 @@ def main():
     sim = SIM.make_sim_tokens(cfg, future_len=(n_steps + 2) * (cfg.max_depth + 1))
     st = VerifyState.build(cfg, tokens=sim.tokens, steps_headroom=n_steps, kv_headroom=n_steps * (cfg.max_depth + 1))
     target = SIM.ContinuationTarget(st, sim.future, sampled=not args.greedy)
+    kv_bytes = 2 * st.k_cache.numel() * st.k_cache.element_size()
+    n_pools = args.kv_pools if args.kv_pools > 0 else (3 if kv_bytes < 256e6 else 1)
+    # rotating copies of the KV cache (same block table and page ids), so a
+    # cache smaller than the 256 MB Infinity Cache is not served from it on
+    # every step; each step attends to and commits into its own pool
+    pools = [(st.k_cache, st.v_cache)] + [(st.k_cache.clone(), st.v_cache.clone()) for _ in range(n_pools - 1)]
+    pool_no = [0]
+
+    def next_pool():
+        st.k_cache, st.v_cache = pools[pool_no[0] % n_pools]
+        pool_no[0] += 1
     torch.cuda.synchronize()
     t_setup = time.perf_counter() - t_setup
     print(f"# setup {t_setup:.1f}s: {cfg.name}, B={st.tokens.batch}", file=sys.stderr, flush=True)
     step_no = [0]
 
     def draft():
+        next_pool()
         st.draft()
         target.apply(st, step_no[0])
         step_no[0] += 1
@@ -532,6 +607,7 @@ def main():
     part_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in parts]
                for _ in range(args.part_steps)]
     for k in range(args.part_steps):
+        next_pool()
         for j, p in enumerate(parts):
             part_ev[k][j][0].record(stream)
             (insert if p == "insert" else getattr(st, p))()
@@ -562,7 +638,7 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": nbytes / t_attn / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = counter_traffic()
+    roof["traffic"] = counter_traffic(cfg.name)
     roof["kernel"] = "srt_tree_attn (tree_attn_plan_kernel + tree_attn_kernel + tree_attn_combine_kernel)"
     roof["algorithmic_bytes"] = nbytes
     roof["algorithmic_flops"] = flops
@@ -595,6 +671,7 @@ def main():
             "seq_len": int(st.tokens.ctx_len.max()),
             "mean_ctx": float(st.tokens.ctx_len.mean()),
             "parallelism": "none (1 GPU)",
+            "kv_pools": n_pools,
         },
         "tree_attn_hbm": {"achieved_GBps": attn_hbm, "peak_GBps": HBM_PEAK_GBPS, "frac": attn_hbm / HBM_PEAK_GBPS},
         "parts_ms": part_ms,
@@ -604,6 +681,8 @@ def main():
         "mean_emitted": n_emit / args.steps / B,
         "roofline": roof,
     }
+    if args.full_tree:
+        res["full_tree"] = [full_tree_attention(st, cfg, int(n)) for n in args.full_tree.split(",") if n]
     if args.head_calls > 0:
         res["fused_head"] = fused_head(st, cfg, args.head_calls, not args.no_unfused)
     if not args.no_bulk:

@@ -137,10 +137,14 @@ class ContinuationTarget:
 
 
 def run(cfg: W.Config, sim: SimTokens, steps: int, strategy: str = "onthefly", alpha: float = 0.0,
-        min_score: float = 0.0, chain: bool = False, n_nodes: Optional[int] = None, device: str = "cuda") -> Dict:
+        min_score: float = 0.0, chain: bool = False, n_nodes: Optional[int] = None, device: str = "cuda",
+        record: bool = False) -> Dict:
     """One simulation: ``strategy`` is "history" (prior rollouts only, no
     online insertion), "onthefly" (running rollouts inserted as they grow)
-    or "runahead" (on-the-fly plus the run-ahead rollouts inserted first)."""
+    or "runahead" (on-the-fly plus the run-ahead rollouts inserted first).
+    With ``record`` the result also holds every step's per-sequence accepted
+    counts and tree sizes ("per_step_accepted", "per_step_nodes", [steps, B]
+    int lists)."""
     if strategy not in ("history", "onthefly", "runahead"):
         raise ValueError(strategy)
     if n_nodes is not None:
@@ -161,8 +165,10 @@ def run(cfg: W.Config, sim: SimTokens, steps: int, strategy: str = "onthefly", a
     acc_sum = torch.zeros(B, dtype=torch.int64, device=device)
     emit_sum = torch.zeros(B, dtype=torch.int64, device=device)
     node_sum = torch.zeros(B, dtype=torch.int64, device=device)
+    rec_acc = torch.zeros((steps, B), dtype=torch.int32, device=device)
+    rec_nodes = torch.zeros((steps, B), dtype=torch.int32, device=device)
     t0 = time.perf_counter()
-    for _ in range(steps):
+    for k in range(steps):
         tree = st.draft(alpha=alpha, min_score=min_score, chain=chain)
         depth = tree["tree_depth"].long().clamp(min=0)
         pos = (used[:, None] + depth).clamp(max=sim.future.shape[1] - 1)
@@ -178,6 +184,9 @@ def run(cfg: W.Config, sim: SimTokens, steps: int, strategy: str = "onthefly", a
         acc_sum += acc["n_accepted"].long()
         emit_sum += acc["n_emitted"].long()
         node_sum += tree["n_nodes"].long()
+        if record:
+            rec_acc[k].copy_(acc["n_accepted"])
+            rec_nodes[k].copy_(tree["n_nodes"])
     torch.cuda.synchronize()
     secs = time.perf_counter() - t0
     # the committed tokens must be the true continuation: check every
@@ -198,6 +207,9 @@ def run(cfg: W.Config, sim: SimTokens, steps: int, strategy: str = "onthefly", a
         "seconds": secs,
     }
     res["accepted_per_drafted"] = res["mean_accepted_per_step"] / max(res["mean_tree_nodes"] - 1.0, 1e-9)
+    if record:
+        res["per_step_accepted"] = rec_acc.cpu().numpy().tolist()
+        res["per_step_nodes"] = rec_nodes.cpu().numpy().tolist()
     del st
     torch.cuda.empty_cache()
     return res
