@@ -679,6 +679,9 @@ def main():
         "accepted_tokens_per_s": n_emit / args.steps / (ms_step / 1e3),
         "mean_tree_nodes": n_tree / args.steps / B,
         "mean_emitted": n_emit / args.steps / B,
+        # sequences still walking at each step of the acceptance walk (mean over timed steps)
+        "accept_walkers_per_level": [round(float(np.mean((re_ > lv).sum(axis=1))), 1)
+                                     for lv in range(cfg.max_depth + 1)],
         "roofline": roof,
     }
     if args.full_tree:

@@ -151,7 +151,19 @@ __device__ inline Best chunk_argmax(const AcceptArgs& a, const float* __restrict
       take(b, score(x.w, g.w, a.invT, kNoise), 4 * i + 3);
     }
   } else {
-    for (int j = lo + tid; j < hi; j += kThreads) take(b, score(row[j], kNoise ? noise[j] : 0.f, a.invT, kNoise), j);
+    int j = lo + tid;
+    for (; j + 7 * kThreads < hi; j += 8 * kThreads) {
+      float x[8], g[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = __builtin_nontemporal_load(&row[j + u * kThreads]);
+      if (kNoise) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) g[u] = __builtin_nontemporal_load(&noise[j + u * kThreads]);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) take(b, score(x[u], kNoise ? g[u] : 0.f, a.invT, kNoise), j + u * kThreads);
+    }
+    for (; j < hi; j += kThreads) take(b, score(row[j], kNoise ? noise[j] : 0.f, a.invT, kNoise), j);
   }
   // lanes, then waves through LDS
 #pragma unroll

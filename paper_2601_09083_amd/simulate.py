@@ -126,7 +126,7 @@ class ContinuationTarget:
         st.logits = self.logits
         if self.noise is not None:
             B, D1, V = self.shape
-            off = (step * 104729) % (D1 * V)
+            off = (step * 104729) % (D1 * V) // 4 * 4  # 16-byte aligned, as a caller's tensor is
             st.gumbel = self.noise.view(-1)[off: off + B * D1 * V].view(B, D1, V)
         else:
             st.gumbel = None

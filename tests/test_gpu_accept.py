@@ -2,7 +2,7 @@
 Gumbel sampling, temperatures, ties, vocabularies with and without 16-byte
 alignment, depth caps, long accepted paths; large vocabularies split over
 up to 32 workgroups per row (chunks), with ties across chunks;
-batches of 70-300 sequences with deep walks, and 4000 sequences that all
+batches of 70-600 sequences with deep walks, and 4000 sequences that all
 walk at least three steps deep."""
 import random
 
@@ -75,6 +75,33 @@ def test_walk_exact(V, sampled, inv_t, boost):
         assert got["n_accepted"].max() >= 2
 
 
+@pytest.mark.parametrize("V,off_l,off_g", [(8192, 1, 3), (152064, 0, 1), (4096, 2, 0)])
+def test_walk_exact_misaligned_rows(V, off_l, off_g):
+    # V a multiple of 4 but logits / noise passed as views 1-3 floats into a
+    # larger buffer: the rows are not 16-byte aligned, so the 4-byte path runs
+    rng = random.Random(V + off_l)
+    B, N, Dmax = 40, 32, 8
+    say(f"accept: misaligned rows V={V} logits +{off_l} noise +{off_g} floats")
+    tree = random_trees(rng, B, N, Dmax, V)
+    cfg = W.Config("acc", 0, n_prompts=B, seqs_per_prompt=1, vocab=V, rollouts_per_prompt=0,
+                   rollout_len=W.Dist("fixed", 1), ctx_len=W.Dist("fixed", 1), n_nodes=N, max_depth=Dmax,
+                   hq=1, hkv=1, head_dim=64, boost_p=0.9, boost_add=40.0)
+    lg = W.make_logits(cfg, tree["tree_tokens"], tree["tree_parent"], tree["n_nodes"], device="cuda", seed=V,
+                       boost="top", sigma=2.0)
+    gm = W.make_gumbel(cfg, B, device="cuda", seed=V + 1)
+    lbuf = torch.empty(lg.numel() + 4, dtype=torch.float32, device="cuda")
+    gbuf = torch.empty(gm.numel() + 4, dtype=torch.float32, device="cuda")
+    logits = lbuf[off_l:off_l + lg.numel()].view(lg.shape)
+    gumbel = gbuf[off_g:off_g + gm.numel()].view(gm.shape)
+    logits.copy_(lg)
+    gumbel.copy_(gm)
+    got = run(tree, logits, gumbel, 1.0, Dmax)
+    want = oracle_accept_rows(lg, gm, 1.0, tree, range(B), Dmax)
+    for b in range(B):
+        assert_accept_equal(got, b, want[b], Dmax)
+    assert got["n_accepted"].max() >= 2
+
+
 def test_depth_cap_and_chain():
     V, Dmax = 64, 3
     N = 10
@@ -118,13 +145,14 @@ def deep_trees(rng, B, N, Dmax, V):
     return {"tree_tokens": tt, "tree_parent": tp, "tree_depth": td, "n_nodes": nn}
 
 
-@pytest.mark.parametrize("B,V,sampled,ties", [(100, 152064, True, False), (100, 152064, False, True),
-                                              (300, 1024, True, False), (70, 50001, False, False)])
-def test_walk_exact_large_batch(B, V, sampled, ties):
+@pytest.mark.parametrize("B,V,sampled,ties,N", [(100, 152064, True, False, 32), (100, 152064, False, True, 32),
+                                                (300, 1024, True, False, 32), (70, 50001, False, False, 32),
+                                                (600, 152064, True, False, 16)])
+def test_walk_exact_large_batch(B, V, sampled, ties, N):
     # a node's last child gets +30 with p = 0.9, so most walks go deep and the
     # late levels run with few walkers left
     rng = random.Random(B * 13 + V)
-    N, Dmax = 32, 12
+    Dmax = 12
     say(f"accept: B={B} V={V} sampled={sampled} ties={ties}")
     tree = deep_trees(rng, B, N, Dmax, V)
     g = torch.Generator(device="cuda")
