@@ -134,7 +134,8 @@ __device__ inline Key frontier_key(const Smem& sm, int e) {
 // the end.  Entries that cannot be selected are dropped as they are found; a
 // round whose children do not fit the pool reports failure.
 // ---------------------------------------------------------------------------
-constexpr int kPool = 1024;     // candidate pool entries (entry 0 is u)
+constexpr int kPool = 2048;     // candidate pool entries (entry 0 is u)
+constexpr int kCompactAt = 512; // pool size above which a round starts with a compaction
 constexpr uint8_t kOpen = 0;    // discovered, children not yet walked
 constexpr uint8_t kDone = 1;    // children walked, or a leaf, or at the depth limit
 constexpr uint8_t kDropped = 2; // cannot be selected
@@ -166,14 +167,18 @@ __device__ inline int rank_below(uint64_t bal) {
 __device__ inline int64_t score_key(double s) { return __double_as_longlong(s); }
 
 // Runs f with a compile-time number of 64-entry chunks per lane covering n
-// entries (n <= kPool).
+// entries (n <= kWide).  Larger pools go through the out-of-line *_wide
+// functions below, so that their register arrays do not weigh on the rest
+// of the kernel.
+constexpr int kWide = 16 * SRT_WAVE;
+
 template <typename F>
 __device__ inline auto by_chunks(int n, F f) {
   if (n <= SRT_WAVE) return f(std::integral_constant<int, 1>{});
   if (n <= 2 * SRT_WAVE) return f(std::integral_constant<int, 2>{});
   if (n <= 4 * SRT_WAVE) return f(std::integral_constant<int, 4>{});
   if (n <= 8 * SRT_WAVE) return f(std::integral_constant<int, 8>{});
-  return f(std::integral_constant<int, kPool / SRT_WAVE>{});
+  return f(std::integral_constant<int, kWide / SRT_WAVE>{});
 }
 
 // c[r] += the number of entries w in 1 .. M-1 scoring strictly above key r.
@@ -262,11 +267,123 @@ __device__ int keep_marks(Pool& P, int lane, int M, int budget) {
   return kept;
 }
 
+// keep_marks without the counts: an entry has fewer than `budget` entries
+// of strictly larger score exactly when its key is at least the
+// `budget`-th largest key t (kth_score_key), so the kept set is the same;
+// pos is left as it was (only the last compaction's counts are used).
+template <int R>
+__device__ int keep_marks_at(Pool& P, int lane, int M, int64_t t) {
+  int kept = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = lane + SRT_WAVE * r;
+    const bool live = i >= 1 && i < M && P.state[i] != kDropped;
+    const bool keep = i == 0 || (live && score_key(P.score[i]) >= t);
+    if (i < M && !keep) P.state[i] = kDropped;
+    const uint64_t bal = __ballot(keep);
+    if (keep) P.aux[i] = static_cast<uint16_t>(kept + rank_below(bal));
+    kept += __popcll(bal);
+  }
+  return kept;
+}
+
+// Pools of more than kWide entries (a round that found many children, or
+// many candidates tied at the budget-th score): the same results as the
+// register-held versions, with at most kWide / SRT_WAVE chunks in registers.
+constexpr int kWideR = kWide / SRT_WAVE;
+
+// kth_score_key: the first kWide entries' keys held here, the rest read
+// from LDS at every bit.
+__device__ int64_t kth_score_key_wide(const Pool& P, int lane, int M, int budget) {
+  int64_t k[kWideR];
+#pragma unroll
+  for (int r = 0; r < kWideR; ++r) {
+    const int i = lane + SRT_WAVE * r;
+    k[r] = i >= 1 && i < M ? score_key(P.score[i]) : -1;
+  }
+  int64_t t = 0;
+  for (int bit = 62; bit >= 0; --bit) {
+    const int64_t c = t | (int64_t{1} << bit);
+    int n = 0;
+#pragma unroll
+    for (int r = 0; r < kWideR; ++r) n += __popcll(__ballot(k[r] >= c));
+    for (int i0 = kWide; i0 < M; i0 += SRT_WAVE) {
+      const int i = i0 + lane;
+      n += __popcll(__ballot(i < M && score_key(P.score[i]) >= c));
+    }
+    if (n >= budget) t = c;
+  }
+  return t;
+}
+
+// keep_marks, kWide entries at a time.
+__device__ int keep_marks_wide(Pool& P, int lane, int M, int budget) {
+  int kept = 0;
+  for (int base = 0; base < M; base += kWide) {
+    int c[kWideR];
+    int64_t ks[kWideR];
+#pragma unroll
+    for (int r = 0; r < kWideR; ++r) {
+      const int i = base + lane + SRT_WAVE * r;
+      const bool live = i >= 1 && i < M && P.state[i] != kDropped;
+      ks[r] = live ? score_key(P.score[i]) : kNoKey;
+      c[r] = 0;
+    }
+    count_above<kWideR>(P, M, ks, c);
+#pragma unroll
+    for (int r = 0; r < kWideR; ++r) {
+      const int i = base + lane + SRT_WAVE * r;
+      const bool keep = i == 0 || (i < M && ks[r] != kNoKey && c[r] < budget);
+      if (i < M && !keep) P.state[i] = kDropped;
+      const uint64_t bal = __ballot(keep);
+      if (keep) {
+        P.aux[i] = static_cast<uint16_t>(kept + rank_below(bal));
+        P.pos[i] = static_cast<uint16_t>(c[r]);
+      }
+      kept += __popcll(bal);
+    }
+  }
+  return kept;
+}
+
+// keep_marks_at over any number of chunks.
+__device__ int keep_marks_at_wide(Pool& P, int lane, int M, int64_t t) {
+  int kept = 0;
+  for (int i0 = 0; i0 < M; i0 += SRT_WAVE) {
+    const int i = i0 + lane;
+    const bool live = i >= 1 && i < M && P.state[i] != kDropped;
+    const bool keep = i == 0 || (live && score_key(P.score[i]) >= t);
+    if (i < M && !keep) P.state[i] = kDropped;
+    const uint64_t bal = __ballot(keep);
+    if (keep) P.aux[i] = static_cast<uint16_t>(kept + rank_below(bal));
+    kept += __popcll(bal);
+  }
+  return kept;
+}
+
+// The budget-th largest score key among entries 1 .. M-1 (kth_score_key).
+__device__ inline int64_t kth_key(const Pool& P, int lane, int M, int budget) {
+  if (M > kWide) return kth_score_key_wide(P, lane, M, budget);
+  return by_chunks(M, [&](auto rc) { return kth_score_key<decltype(rc)::value>(P, lane, M, budget); });
+}
+
 // Keeps entry 0 and every entry that can still be selected, moved down in
 // index order.  A kept entry's parent is kept too (it scores at least as
-// high), and stays ahead of it.  Returns the new entry count.
-__device__ __forceinline__ int compact(Pool& P, int lane, int M, int budget) {
-  const int kept = by_chunks(M, [&](auto rc) { return keep_marks<decltype(rc)::value>(P, lane, M, budget); });
+// high), and stays ahead of it.  With `counts`, each kept entry's count of
+// entries scoring strictly higher goes to pos (the final compaction);
+// without, the kept set comes from the budget-th largest score (a round's
+// compaction, where only the set matters).  Returns the new entry count.
+__device__ __forceinline__ int compact(Pool& P, int lane, int M, int budget, bool counts) {
+  int kept;
+  if (M > kWide) {
+    kept = counts ? keep_marks_wide(P, lane, M, budget) : keep_marks_at_wide(P, lane, M, kth_key(P, lane, M, budget));
+  } else {
+    kept = by_chunks(M, [&](auto rc) {
+      constexpr int R = decltype(rc)::value;
+      if (counts || M - 1 <= budget) return keep_marks<R>(P, lane, M, budget);
+      return keep_marks_at<R>(P, lane, M, kth_score_key<R>(P, lane, M, budget));
+    });
+  }
   __syncthreads();
   if (kept < M) {
     // chunk by chunk: a chunk's new indices lie below its own range and above
@@ -325,7 +442,7 @@ __device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_hea
   __syncthreads();
   int M = 1;
   for (;;) {
-    if (M > kPool / 2) M = compact(P, lane, M, budget);
+    if (M > kCompactAt) M = compact(P, lane, M, budget, false);
     // List the open entries, then drop those that can no longer be selected.
     int n_open = 0;
     for (int base = 0; base < M; base += SRT_WAVE) {
@@ -337,7 +454,7 @@ __device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_hea
     }
     if (n_open > 0 && M - 1 > budget) {
       __syncthreads();
-      const int64_t t = by_chunks(M, [&](auto rc) { return kth_score_key<decltype(rc)::value>(P, lane, M, budget); });
+      const int64_t t = kth_key(P, lane, M, budget);
       n_open = drop_below(P, lane, n_open, t);
     }
     if (n_open == 0) break;
@@ -388,7 +505,7 @@ __device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_hea
   }
 
   __syncthreads();
-  M = compact(P, lane, M, budget);
+  M = compact(P, lane, M, budget, true);
 
   // Entries 1 .. M-1 listed by depth (counting sort).
   P.dcount[lane] = 0;

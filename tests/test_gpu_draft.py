@@ -1,9 +1,11 @@
 """GPU parity of srt_draft against the oracle draft, bit-exact: the tiny
 configuration, random small-vocabulary caches full of score ties, budget and
 depth variants, score thresholds and chain drafts, fallbacks, a candidate pool
-pruned while more than half full, and a 1500-child list that overflows the
-pool (the one-at-a-time path then runs, its frontier evicting; also with chain
-drafts)."""
+pruned while more than a quarter full, a 1500-child list that takes the pool
+past 1024 entries (the wide-pool selection and pruning), 1500 children tied
+in score that keep it there up to the final pruning, and a 3000-child list
+that overflows the 2048-entry pool (the one-at-a-time path then runs, its
+frontier evicting; also with chain drafts)."""
 import random
 
 import numpy as np
@@ -67,24 +69,46 @@ def test_random_small_vocab_ties(seed):
             assert_tree_equal(tree, b, want)
 
 
-def test_frontier_overflow_and_long_child_lists():
-    # node (7) has 1500 children of unequal counts: the frontier (512) must
-    # evict without losing any of the best 255 candidates
+@pytest.mark.parametrize("n_children", [1500, 3000])
+def test_frontier_overflow_and_long_child_lists(n_children):
+    # node (7) has up to n_children children of unequal counts.  1500 fit the
+    # 2048-entry pool, which then holds more than 1024 entries (the wide-pool
+    # selection and pruning); 3000 overflow it, and the one-at-a-time path's
+    # frontier (512) must evict without losing any of the best 255 candidates
     rng = np.random.default_rng(0)
     D = 6
-    streams = [[np.array([7, int(x), int(y)]) for x, y in zip(rng.integers(0, 1500, size=4000),
-                                                               rng.integers(0, 3, size=4000))]]
-    c = Caches.create(1, 4001, D, 100000)
-    c.insert([0] * 4000, c.new_streams(4000), streams[0])
+    n_str = 8000 if n_children > 2000 else 4000
+    streams = [[np.array([7, int(x), int(y)]) for x, y in zip(rng.integers(0, n_children, size=n_str),
+                                                               rng.integers(0, 3, size=n_str))]]
+    c = Caches.create(1, n_str + 1, D, 200000)
+    c.insert([0] * n_str, c.new_streams(n_str), streams[0])
     trie = TR.DictTrie(TR.substring_counts(streams[0], D), D)
     for N, Dmax in [(256, 2), (256, 1), (100, 2)]:
-        say(f"draft: frontier overflow N={N} Dmax={Dmax}")
+        say(f"draft: {n_children} children N={N} Dmax={Dmax}")
         tree = run_draft(c, [0], [[7]], [5], 1, N, Dmax)
         assert_tree_equal(tree, 0, DR.draft(trie, [7], 5, 1, N, Dmax))
     for tau, chain in [(0.0, True), (1e-4, False), (1e-3, True)]:
-        say(f"draft: long child list tau={tau} chain={chain}")
+        say(f"draft: {n_children} children tau={tau} chain={chain}")
         tree = run_draft(c, [0], [[7]], [5], 1, 256, 2, 0.0, tau, chain)
         assert_tree_equal(tree, 0, DR.draft(trie, [7], 5, 1, 256, 2, 0.0, tau, chain))
+
+
+def test_wide_pool_ties_to_the_final_pruning():
+    # node (7) has 1500 children with 2 occurrences each: every child scores
+    # 1/1500, so all of them tie at the budget-th score and are kept; the pool
+    # keeps 1501 entries through the final pruning (whose counts then run
+    # over two register passes), and the tie order (token ascending) decides
+    # which 255 are drafted.  With Dmax = 2 their children (one each) come too.
+    D = 6
+    streams = [np.array([7, 1000 + x, 5000 + x]) for x in range(1500) for _ in range(2)]
+    c = Caches.create(1, len(streams) + 1, D, 200000)
+    c.insert([0] * len(streams), c.new_streams(len(streams)), streams)
+    trie = TR.DictTrie(TR.substring_counts(streams, D), D)
+    for N, Dmax in [(256, 1), (256, 2), (64, 2)]:
+        say(f"draft: 1500 tied children N={N} Dmax={Dmax}")
+        tree = run_draft(c, [0], [[7]], [5], 1, N, Dmax)
+        assert_tree_equal(tree, 0, DR.draft(trie, [7], 5, 1, N, Dmax))
+        assert int(tree["n_nodes"][0]) == N
 
 
 def test_pool_over_half_full():
@@ -92,7 +116,8 @@ def test_pool_over_half_full():
     # counts repeat with period 13, so scores tie in groups); each grandchild
     # has up to 3 children.  Drafting 63 nodes first discovers all 560
     # grandchildren, so the candidate pool passes 512 entries and is pruned to
-    # what can still be selected before the next level is walked.
+    # what can still be selected (at the budget-th score) before the next
+    # level is walked.
     rng = np.random.default_rng(5)
     streams = []
     for a in range(8):
