@@ -153,6 +153,7 @@ struct Pool {
   uint8_t depth[kPool];
   uint8_t state[kPool];
   uint32_t dcount[64];            // entries per depth (then per depth slot)
+  uint32_t tcount[64];            // candidates tied at the cut's score, per depth
   uint32_t dstart[64];            // first list slot of each depth
   uint32_t m;                     // entries in use; appends reserve slots here
 };
@@ -217,30 +218,87 @@ __device__ int64_t kth_score_key(const Pool& P, int lane, int M, int budget) {
   return t;
 }
 
-// Drops the n listed open entries whose score key is below t (they have
-// `budget` or more entries of strictly larger score) and compacts the list in
-// place; returns its new length.
-__device__ int drop_below(Pool& P, int lane, int n, int64_t t) {
+// Which candidates can still be selected.  An entry has fewer than `budget`
+// entries of strictly larger score exactly when its key is at least t, the
+// `budget`-th largest key (kth_score_key).  Entries of equal score rank by
+// depth first, so an entry scoring exactly t at depth d has, strictly ahead
+// of it, every entry scoring above t and every entry scoring t at a smaller
+// depth; it stays selectable while those number fewer than `budget`, i.e.
+// while d <= dmax.  Adding entries only moves entries back, so whatever is
+// not selectable never becomes so; and a selectable entry's parent is
+// selectable too (it scores at least as much, at a smaller depth).
+struct Cut {
+  int64_t t;
+  int dmax;
+};
+
+constexpr Cut kNoCut{INT64_MIN, 63};  // every entry (fewer entries than the budget)
+
+__device__ inline bool selectable(int64_t key, int depth, const Cut& c) {
+  return key > c.t || (key == c.t && depth <= c.dmax);
+}
+
+__device__ inline int64_t kth_key(const Pool& P, int lane, int M, int budget);
+
+// The cut for entries 1 .. M-1 (M - 1 > budget): t, then one pass that
+// counts the entries scoring above t and, per depth, those scoring t (the
+// same entries kth_score_key counts, whatever their state: an entry dropped
+// earlier either scores below t now or lies deeper than any depth it
+// could change).
+__device__ Cut cut_of(Pool& P, int lane, int M, int budget) {
+  Cut c{kth_key(P, lane, M, budget), 63};
+  P.tcount[lane] = 0;
+  __syncthreads();
+  int above = 0;
+  for (int i0 = 0; i0 < M; i0 += SRT_WAVE) {
+    const int i = i0 + lane;
+    const int64_t k = i >= 1 && i < M ? score_key(P.score[i]) : INT64_MIN;
+    above += __popcll(__ballot(k > c.t));
+    if (k == c.t) atomicAdd(&P.tcount[P.depth[i]], 1u);
+  }
+  __syncthreads();
+  const int cnt = static_cast<int>(P.tcount[lane]);  // lane = depth
+  int incl = cnt;
+#pragma unroll
+  for (int off = 1; off < SRT_WAVE; off <<= 1) {
+    const int o = __shfl_up(incl, off, SRT_WAVE);
+    if (lane >= off) incl += o;
+  }
+  // tied entries shallower than depth `lane`, plus those above t
+  const uint64_t ok = __ballot(above + incl - cnt < budget);
+  c.dmax = 63 - __clzll(static_cast<long long>(ok));
+  return c;
+}
+
+// Drops the n listed open entries that cannot be selected any more (see
+// Cut), closes those that can but whose children cannot (scoring exactly t
+// at depth dmax or deeper: a child scores at most as much, one level
+// deeper), and compacts the list in place to the entries still to expand;
+// returns its new length.
+__device__ int drop_below(Pool& P, int lane, int n, const Cut& cut) {
   int kept = 0;
   for (int base = 0; base < n; base += SRT_WAVE) {
     const int j = base + lane;
     const int i = j < n ? P.list[j] : -1;
-    const bool keep = i >= 0 && score_key(P.score[i]) >= t;
+    const int64_t k = i >= 0 ? score_key(P.score[i]) : 0;
+    const int d = i >= 0 ? P.depth[i] : 0;
+    const bool sel = i >= 0 && selectable(k, d, cut);
+    const bool keep = sel && !(k == cut.t && d >= cut.dmax);
     const uint64_t bal = __ballot(keep);  // every lane has read its entry
     if (keep) P.list[kept + rank_below(bal)] = static_cast<uint16_t>(i);
-    else if (i >= 0) P.state[i] = kDropped;
+    else if (i >= 0) P.state[i] = sel ? kDone : kDropped;
     kept += __popcll(bal);
   }
   return kept;
 }
 
 // Marks for keeping entry 0 and every entry that can still be selected (not
-// dropped, fewer than `budget` entries of strictly larger score), drops the
-// rest, writes each kept entry's new index to aux and its count of entries
-// scoring strictly higher to pos; returns the number kept.  Every entry
-// scoring above a kept one is kept too, so the count holds after compaction.
+// dropped, selectable under the cut), drops the rest, writes each kept
+// entry's new index to aux and its count of entries scoring strictly higher
+// to pos; returns the number kept.  Every entry scoring above a kept one is
+// kept too, so the count holds after compaction.
 template <int R>
-__device__ int keep_marks(Pool& P, int lane, int M, int budget) {
+__device__ int keep_marks(Pool& P, int lane, int M, const Cut& cut) {
   int c[R];
   int64_t ks[R];
 #pragma unroll
@@ -255,7 +313,7 @@ __device__ int keep_marks(Pool& P, int lane, int M, int budget) {
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int i = lane + SRT_WAVE * r;
-    const bool keep = i == 0 || (i < M && ks[r] != kNoKey && c[r] < budget);
+    const bool keep = i == 0 || (i < M && ks[r] != kNoKey && selectable(ks[r], P.depth[i], cut));
     if (i < M && !keep) P.state[i] = kDropped;
     const uint64_t bal = __ballot(keep);
     if (keep) {
@@ -267,18 +325,16 @@ __device__ int keep_marks(Pool& P, int lane, int M, int budget) {
   return kept;
 }
 
-// keep_marks without the counts: an entry has fewer than `budget` entries
-// of strictly larger score exactly when its key is at least the
-// `budget`-th largest key t (kth_score_key), so the kept set is the same;
-// pos is left as it was (only the last compaction's counts are used).
+// keep_marks without the counts (a round's compaction, where only the kept
+// set matters); pos is left as it was.
 template <int R>
-__device__ int keep_marks_at(Pool& P, int lane, int M, int64_t t) {
+__device__ int keep_marks_at(Pool& P, int lane, int M, const Cut& cut) {
   int kept = 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int i = lane + SRT_WAVE * r;
     const bool live = i >= 1 && i < M && P.state[i] != kDropped;
-    const bool keep = i == 0 || (live && score_key(P.score[i]) >= t);
+    const bool keep = i == 0 || (live && selectable(score_key(P.score[i]), P.depth[i], cut));
     if (i < M && !keep) P.state[i] = kDropped;
     const uint64_t bal = __ballot(keep);
     if (keep) P.aux[i] = static_cast<uint16_t>(kept + rank_below(bal));
@@ -317,7 +373,7 @@ __device__ int64_t kth_score_key_wide(const Pool& P, int lane, int M, int budget
 }
 
 // keep_marks, kWide entries at a time.
-__device__ int keep_marks_wide(Pool& P, int lane, int M, int budget) {
+__device__ int keep_marks_wide(Pool& P, int lane, int M, const Cut& cut) {
   int kept = 0;
   for (int base = 0; base < M; base += kWide) {
     int c[kWideR];
@@ -333,7 +389,7 @@ __device__ int keep_marks_wide(Pool& P, int lane, int M, int budget) {
 #pragma unroll
     for (int r = 0; r < kWideR; ++r) {
       const int i = base + lane + SRT_WAVE * r;
-      const bool keep = i == 0 || (i < M && ks[r] != kNoKey && c[r] < budget);
+      const bool keep = i == 0 || (i < M && ks[r] != kNoKey && selectable(ks[r], P.depth[i], cut));
       if (i < M && !keep) P.state[i] = kDropped;
       const uint64_t bal = __ballot(keep);
       if (keep) {
@@ -347,12 +403,12 @@ __device__ int keep_marks_wide(Pool& P, int lane, int M, int budget) {
 }
 
 // keep_marks_at over any number of chunks.
-__device__ int keep_marks_at_wide(Pool& P, int lane, int M, int64_t t) {
+__device__ int keep_marks_at_wide(Pool& P, int lane, int M, const Cut& cut) {
   int kept = 0;
   for (int i0 = 0; i0 < M; i0 += SRT_WAVE) {
     const int i = i0 + lane;
     const bool live = i >= 1 && i < M && P.state[i] != kDropped;
-    const bool keep = i == 0 || (live && score_key(P.score[i]) >= t);
+    const bool keep = i == 0 || (live && selectable(score_key(P.score[i]), P.depth[i], cut));
     if (i < M && !keep) P.state[i] = kDropped;
     const uint64_t bal = __ballot(keep);
     if (keep) P.aux[i] = static_cast<uint16_t>(kept + rank_below(bal));
@@ -367,21 +423,21 @@ __device__ inline int64_t kth_key(const Pool& P, int lane, int M, int budget) {
   return by_chunks(M, [&](auto rc) { return kth_score_key<decltype(rc)::value>(P, lane, M, budget); });
 }
 
-// Keeps entry 0 and every entry that can still be selected, moved down in
-// index order.  A kept entry's parent is kept too (it scores at least as
-// high), and stays ahead of it.  With `counts`, each kept entry's count of
-// entries scoring strictly higher goes to pos (the final compaction);
-// without, the kept set comes from the budget-th largest score (a round's
-// compaction, where only the set matters).  Returns the new entry count.
+// Keeps entry 0 and every entry that can still be selected (see Cut), moved
+// down in index order.  A kept entry's parent is kept too, and stays ahead
+// of it.  With `counts`, each kept entry's count of entries scoring strictly
+// higher goes to pos (the final compaction); without, only the kept set is
+// made (a round's compaction).  Returns the new entry count.
 __device__ __forceinline__ int compact(Pool& P, int lane, int M, int budget, bool counts) {
+  const Cut cut = M - 1 > budget ? cut_of(P, lane, M, budget) : kNoCut;
   int kept;
   if (M > kWide) {
-    kept = counts ? keep_marks_wide(P, lane, M, budget) : keep_marks_at_wide(P, lane, M, kth_key(P, lane, M, budget));
+    kept = counts ? keep_marks_wide(P, lane, M, cut) : keep_marks_at_wide(P, lane, M, cut);
   } else {
     kept = by_chunks(M, [&](auto rc) {
       constexpr int R = decltype(rc)::value;
-      if (counts || M - 1 <= budget) return keep_marks<R>(P, lane, M, budget);
-      return keep_marks_at<R>(P, lane, M, kth_score_key<R>(P, lane, M, budget));
+      if (counts) return keep_marks<R>(P, lane, M, cut);
+      return keep_marks_at<R>(P, lane, M, cut);
     });
   }
   __syncthreads();
@@ -454,8 +510,7 @@ __device__ int draft_levels(const TrieView& t, Pool& P, int lane, uint32_t u_hea
     }
     if (n_open > 0 && M - 1 > budget) {
       __syncthreads();
-      const int64_t t = kth_key(P, lane, M, budget);
-      n_open = drop_below(P, lane, n_open, t);
+      n_open = drop_below(P, lane, n_open, cut_of(P, lane, M, budget));
     }
     if (n_open == 0) break;
     __syncthreads();

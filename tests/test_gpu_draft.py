@@ -98,7 +98,9 @@ def test_wide_pool_ties_to_the_final_pruning():
     # 1/1500, so all of them tie at the budget-th score and are kept; the pool
     # keeps 1501 entries through the final pruning (whose counts then run
     # over two register passes), and the tie order (token ascending) decides
-    # which 255 are drafted.  With Dmax = 2 their children (one each) come too.
+    # which 255 are drafted.  With Dmax = 2 their children (one each, tied
+    # with them one level deeper) could never be selected, so they are not
+    # walked.
     D = 6
     streams = [np.array([7, 1000 + x, 5000 + x]) for x in range(1500) for _ in range(2)]
     c = Caches.create(1, len(streams) + 1, D, 200000)
