@@ -217,9 +217,9 @@ int srt_tree_attn(int32_t B, int32_t N, int32_t Hq, int32_t Hkv, int32_t d, int3
  * of tokens the sequence appends (ready as `lengths` for srt_trie_insert
  * with tokens = out_tokens, stride Dmax+1).  Inputs must be finite (results
  * are unspecified otherwise).
- * The batch walks one step per kernel (Dmax + 1 level kernels and a last
- * step kernel are always enqueued; a level with no walking sequence exits
- * at once).
+ * The batch walks one step per kernel (Dmax + 1 level kernels, the first
+ * of which also resets the walk's state, and a last step kernel are always
+ * enqueued; a level with no walking sequence exits at once).
  * scratch: device buffer, 256-byte aligned, of at least
  * srt_accept_scratch_bytes(B) bytes (else SRT_ERR_CAPACITY): per-step
  * lists of the walking sequences, their current nodes and per-chunk arg-max

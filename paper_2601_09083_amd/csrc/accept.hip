@@ -24,10 +24,12 @@
 //   * The step's decision is folded into the next level's kernel: every
 //     block of a walker first takes the largest candidate of the walker's
 //     previous row, looks for the child that carries the token (all blocks
-//     of the walker reach the same answer), and one of them writes the
+//     of the walker reach the same answer; the node count and the tree
+//     row load together with the candidates), and one of them writes the
 //     step's output and, if it descends, appends the sequence to the next
 //     level's list; then each block reads its chunk of the child's row.  A
-//     last walk kernel decides the final level.  Candidates and current
+//     last walk kernel decides the final level, and the level-0 kernel
+//     resets the walk's state (no separate launch).  Candidates and current
 //     nodes alternate between two buffers by level parity, so no launch
 //     reads a buffer it writes.
 // x = fl(fl(l * inv_T) + g) is evaluated with explicitly rounded multiply
@@ -184,22 +186,6 @@ __device__ inline Best chunk_argmax(const AcceptArgs& a, const float* __restrict
   return b;
 }
 
-// Outputs to -1; sequence b walks from its root; level counters: every
-// sequence walks at level 0, none yet at later ones (block 0).
-__global__ __launch_bounds__(256) void accept_init_kernel(AcceptArgs a) {
-  if (blockIdx.x == 0)
-    for (int i = threadIdx.x; i <= kMaxLevels; i += 256) a.n_act[i] = i == 0 ? a.B : 0;
-  const int b = blockIdx.x * 256 + threadIdx.x;
-  if (b >= a.B) return;
-  const int64_t row = static_cast<int64_t>(b) * (a.Dmax + 1);
-  for (int k = 0; k <= a.Dmax; ++k) {
-    a.out_tokens[row + k] = -1;
-    a.out_nodes[row + k] = -1;
-  }
-  a.act[b] = b;
-  a.cur[b] = 0;  // level 0, parity 0
-}
-
 // The decision of step `level` for sequence b standing on node u, from the
 // candidates of its row, in one wave: the token, and the child that carries
 // it (-1 if none or if the walk is at its depth cap).
@@ -209,6 +195,12 @@ struct Step {
 
 __device__ inline Step decide(const AcceptArgs& a, int b, int u, int level, int lane) {
   const unsigned long long* cand = a.cand + (static_cast<int64_t>(level & 1) * a.B + b) * kMaxChunks;
+  const int64_t tr = static_cast<int64_t>(b) * a.N;
+  // the node count and the tree row's first 64 nodes load together with the
+  // candidates (their addresses do not depend on the step's token)
+  const int n = min(max(a.n_nodes[b], 1), a.N);
+  const int32_t par0 = lane < a.N ? a.tree_parent[tr + lane] : -1;
+  const int32_t tok0 = lane < a.N ? a.tree_tokens[tr + lane] : -1;
   unsigned long long best = lane < a.n_chunks ? cand[lane] : 0ull;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
@@ -216,13 +208,13 @@ __device__ inline Step decide(const AcceptArgs& a, int b, int u, int level, int 
     best = o > best ? o : best;
   }
   Step st{key_token(best), -1};
-  const int n = min(max(a.n_nodes[b], 1), a.N);
-  const int64_t tr = static_cast<int64_t>(b) * a.N;
-  if (level < a.Dmax) {
-    for (int c0 = u + 1; c0 < n && st.child < 0; c0 += SRT_WAVE) {
+  if (level < a.Dmax) {  // children of u have larger indices
+    unsigned long long m = __ballot(lane > u && lane < n && par0 == u && tok0 == st.tok);
+    if (m) st.child = __ffsll(static_cast<long long>(m)) - 1;
+    for (int c0 = SRT_WAVE; c0 < n && st.child < 0; c0 += SRT_WAVE) {
       const int cc = c0 + lane;
-      const bool hit = cc < n && a.tree_parent[tr + cc] == u && a.tree_tokens[tr + cc] == st.tok;
-      const unsigned long long m = __ballot(hit);
+      const bool hit = cc > u && cc < n && a.tree_parent[tr + cc] == u && a.tree_tokens[tr + cc] == st.tok;
+      m = __ballot(hit);
       if (m) st.child = c0 + __ffsll(static_cast<long long>(m)) - 1;
     }
   }
@@ -253,12 +245,26 @@ __global__ __launch_bounds__(kThreads) void accept_level_kernel(AcceptArgs a, in
   const int g = blockIdx.x;
   const int slot = g / a.n_chunks, c = g - slot * a.n_chunks;
   const int lv = level > 0 ? level - 1 : 0;  // the list the walker comes from
-  if (slot >= a.n_act[lv]) return;
-  const int b = min(max(a.act[(lv & 1) * a.B + slot], 0), a.B - 1);
-  int u;
-  if (level == 0) {
+  int b, u;
+  if (level == 0) {  // every sequence; the walk's state is reset here
+    if (slot >= a.B) return;
+    b = slot;
     u = 0;
+    if (g == 0 && threadIdx.x <= kMaxLevels) a.n_act[threadIdx.x] = threadIdx.x == 0 ? a.B : 0;
+    if (c == 0) {
+      const int64_t orow = static_cast<int64_t>(b) * (a.Dmax + 1);
+      for (int k = threadIdx.x; k <= a.Dmax; k += kThreads) {
+        a.out_tokens[orow + k] = -1;
+        a.out_nodes[orow + k] = -1;
+      }
+      if (threadIdx.x == 0) {
+        a.act[b] = b;  // level 0, parity 0
+        a.cur[b] = 0;
+      }
+    }
   } else {
+    if (slot >= a.n_act[lv]) return;
+    b = min(max(a.act[(lv & 1) * a.B + slot], 0), a.B - 1);
     __shared__ int s_child;
     if (threadIdx.x < SRT_WAVE) {
       const int prev = min(max(a.cur[(lv & 1) * a.B + b], 0), a.N - 1);
@@ -304,7 +310,7 @@ int check_args(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logit
 }
 
 // The walk itself on scratch memory `base` (device, 256-byte aligned, at
-// least scratch_layout(B).total bytes); the init kernel resets the level
+// least scratch_layout(B).total bytes); the level-0 kernel resets the level
 // counters, so the scratch contents on entry do not matter.
 int launch_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* logits, const float* gumbel,
                   float inv_temperature, const int32_t* tree_tokens, const int32_t* tree_parent,
@@ -340,8 +346,7 @@ int launch_accept(int32_t B, int32_t N, int32_t V, int32_t Dmax, const float* lo
   if (grid > 0x7FFFFFFF) return SRT_ERR_UNSUPPORTED;
 
   hipStream_t s = as_stream(stream);
-  accept_init_kernel<<<(B + 255) / 256, 256, 0, s>>>(a);
-  int st = launch_status();
+  int st = SRT_OK;
   const unsigned walk_grid = static_cast<unsigned>((B + kWalkWaves - 1) / kWalkWaves);
   for (int level = 0; level <= Dmax && st == SRT_OK; ++level) {
     if (gumbel)
