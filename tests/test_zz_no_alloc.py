@@ -4,7 +4,9 @@ scratch) through the C ABI: identical outputs, bit for bit, on consecutive
 calls of decreasing size -- the largest batch the array holds, then smaller
 ones with other tree sizes, vocabularies (one not a multiple of 4) and depth
 caps, sampled and greedy -- so that the array's contents from an earlier,
-larger call cannot leak into a later one."""
+larger call cannot leak into a later one; and the same walk captured in a
+HIP graph, replayed three times with other no-alloc calls in between (each
+overwriting the shared array), every replay equal to the eager result."""
 import numpy as np
 import pytest
 import torch
@@ -61,3 +63,34 @@ def test_noalloc_matches_scratch_entry_point():
         emitted = got["n_emitted"].cpu().numpy()
         assert emitted.min() >= 1 and emitted.max() >= min(3, Dmax + 1), "walks should go deep"
         say(f"  equal; emitted per sequence {emitted.mean():.2f}, deepest {emitted.max()}")
+
+
+def test_noalloc_under_graph_capture():
+    B, N, V, Dmax = 300, 32, 4096, 8
+    logits, gumbel, tt, tp, nn = problem(11, B, N, V, Dmax, True)
+    want = srt.srt_accept(logits, gumbel, 1.0, tt, tp, nn, Dmax)
+    out = outputs(B, Dmax)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # first call (and the array's address lookup) outside the capture
+        srt.srt_accept_noalloc(logits, gumbel, 1.0, tt, tp, nn, Dmax, out=out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    say(f"no-alloc accept under graph capture: B={B} N={N} V={V} Dmax={Dmax}")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        srt.srt_accept_noalloc(logits, gumbel, 1.0, tt, tp, nn, Dmax, out=out)
+    torch.cuda.synchronize()
+    o_l, o_g, o_tt, o_tp, o_nn = problem(12, 64, 16, 2000, 5, False)
+    for r in range(3):
+        for v in out.values():
+            v.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in want:
+            assert torch.equal(out[k], want[k]), f"replay {r}: {k} differs"
+        # eager work between replays: another walk through the same array
+        srt.srt_accept_noalloc(o_l, o_g, 1.0, o_tt, o_tp, o_nn, 5, out=outputs(64, 5))
+        torch.cuda.synchronize()
+    say("  three replays equal the eager walk")
