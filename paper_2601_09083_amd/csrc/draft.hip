@@ -124,11 +124,13 @@ __device__ inline Key frontier_key(const Smem& sm, int e) {
 // and no node ranks above its parent (its score is at most the parent's, its
 // depth larger).  So the candidates can be discovered a level at a time: keep
 // a pool of discovered candidates and, in each round, expand every pool entry
-// not yet expanded that has fewer than `budget` entries of strictly larger
-// score.  When a round finds no such entry the pool holds the best `budget`
-// candidates: an undiscovered candidate v has a discovered ancestor a that was
-// never expanded, so at least `budget` candidates score strictly above a and
-// therefore rank strictly above v.  Each round adds the next level of the
+// not yet expanded that ranks, by (score, depth), behind fewer than `budget`
+// entries, and whose children could too (see Cut).  When a round finds no
+// such entry the pool holds the best `budget` candidates: an undiscovered
+// candidate v has a discovered ancestor a that was never expanded, so at
+// least `budget` candidates rank strictly above a by (score, depth), or above
+// any child of a, and therefore strictly above v (which scores at most as
+// much as a, deeper).  Each round adds the next level of the
 // final tree, so the rounds follow the tree depth rather than the node count.
 // The order itself (lexicographic token paths break ties) is computed once at
 // the end.  Entries that cannot be selected are dropped as they are found; a
