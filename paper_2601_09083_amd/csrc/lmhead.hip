@@ -223,6 +223,10 @@ struct Narrow {
 struct Wide {
   static constexpr int WV = 2, VT = 2, WS = 2, ST = 2, TM = 128;
 };
+static_assert(Narrow::WV * Narrow::WS * SRT_WAVE == kThreads && Wide::WV * Wide::WS * SRT_WAVE == kThreads,
+              "the WV x WS waves of either layout fill the workgroup");
+static_assert(Narrow::TM == 32 * Narrow::WS * Narrow::ST && Wide::TM == 32 * Wide::WS * Wide::ST,
+              "TM = 32 WS ST sequences");
 constexpr int kMaxTM = 128;
 constexpr int kWideAbove = 64;  // rows of a level above which it runs wide
 

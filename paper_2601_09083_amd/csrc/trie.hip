@@ -152,7 +152,7 @@ __global__ __launch_bounds__(1024) void insert_kernel(void* ws, const int32_t* _
   // length j (j = 1..m).
   const int m = s_m;
   int32_t* rec = s_rec;
-  if (threadIdx.x < m) s_act[threadIdx.x] = static_cast<uint32_t>(rec[kStreamHead + threadIdx.x]);
+  if (static_cast<int>(threadIdx.x) < m) s_act[threadIdx.x] = static_cast<uint32_t>(rec[kStreamHead + threadIdx.x]);
   __syncthreads();
 
   const uint32_t root = t.roots[p];
